@@ -1,0 +1,191 @@
+"""Benchmark of the libmalt MALT / MALTER step on one MI355X.
+
+Default workload: the GPT-2 Large matrix set (36 blocks, width 1280: 144
+matrices, 707,788,800 fp32 parameters), MALT, 10 consecutive steps timed end
+to end with persistent state, fresh seeded gradients per step.  Inputs are
+drawn on the GPU before the timed region (synthetic: no dataset).
+
+Prints one JSON line:  step latency (value, ms per step), the Newton-Schulz
+GEMM kernel against the bf16 matrix-core peak (roofline), per-kernel achieved
+HBM bandwidth / throughput, and the fp64 CPU oracle timed on a bounded sample
+of the same workload (cpu_baseline).
+
+  python bench.py [--steps K] [--warmup W] [--workload gpt2_large|gpt2_small|gpt2_medium|single_256x512|stress_4096]
+                  [--no-cpu-baseline] [--gpus 1]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 matrix-core peak
+PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
+METRIC = "MALT step latency (ms) per GPT-2 param set; NS MFMA % bf16 peak; HBM GB/s"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="gpt2_large")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-layers", type=int, default=1)
+    return ap.parse_args()
+
+
+def cpu_baseline(w, layers: int):
+    """Time the fp64 oracle (as it stands) on `layers` transformer blocks' worth
+    of matrices (one matrix of every shape per block) and scale per shape to
+    one full step of the workload."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import OracleHparams, oracle_init, oracle_step
+    from paper_2608_05088_amd import workloads as wl
+
+    shapes = list(w.shapes)
+    uniq = []
+    for s in shapes:
+        if s not in uniq:
+            uniq.append(s)
+    per_shape = {}
+    sample_desc = []
+    for s in uniq:
+        idx = shapes.index(s)
+        times = []
+        for rep in range(layers):
+            i = idx + rep * len(uniq) if idx + rep * len(uniq) < len(shapes) else idx
+            G = wl.grad(w.cid, 1, i, s, w.dist)
+            W0 = wl.weight(w.cid, i, s).astype(np.float64)
+            st = oracle_init([s], w.variant)
+            hp = OracleHparams(variant=w.variant, lr=w.lr, mu1=w.mu1, mu2=w.mu2, eps=w.eps)
+            t0 = time.perf_counter()
+            oracle_step([W0], [G], st, hp)
+            times.append(time.perf_counter() - t0)
+        per_shape[s] = sum(times) / len(times)
+        sample_desc.append(f"{s[0]}x{s[1]}")
+    total_s = sum(per_shape[s] for s in shapes)
+    sampled_s = sum(per_shape[s] * layers for s in uniq)
+    threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    return {"value": total_s * 1e3, "unit": "ms per step (extrapolated per shape)", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"one oracle step on {layers} matrix of each shape ({', '.join(sample_desc)}), "
+                      f"{sampled_s:.1f} s of CPU time, scaled by shape counts to all {len(shapes)} matrices",
+            "host_cpus": os.cpu_count()}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (the step shards by whole matrices; see the design notes); "
+              f"--gpus {args.gpus} is not supported", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2608_05088_amd import libmalt as lm
+    from paper_2608_05088_amd import workloads as wl
+
+    byname = {w.name: w for w in wl.WORKLOADS.values()}
+    w = byname[args.workload]
+    K = args.steps if args.steps is not None else max(w.steps, 10 if w.cid == 4 else 5)
+    Wu = args.warmup
+    dev = torch.device("cuda:0")
+    lm.lib()
+    shapes = list(w.shapes)
+    print(f"[bench] workload {w.name}: {len(shapes)} matrices, {w.numel} params, {w.variant}, "
+          f"steps {K} warmup {Wu}", file=sys.stderr, flush=True)
+
+    # Inputs resident in HBM before timing: weights + one fresh gradient set per step.
+    Wd = [wl.weight_device(w.cid, i, s, dev) for i, s in enumerate(shapes)]
+    grad_sets = []
+    for t in range(1, Wu + K + 1):
+        grad_sets.append([wl.grad_device(w.cid, t, i, s, w.dist, dev) for i, s in enumerate(shapes)])
+    torch.cuda.synchronize()
+    print(f"[bench] inputs ready ({torch.cuda.memory_allocated() / 2**30:.1f} GiB)", file=sys.stderr, flush=True)
+
+    plan = lm.Plan(shapes, w.variant, device=dev)
+    hp = lm.make_hparams(lr=w.lr, mu1=w.mu1, mu2=w.mu2, eps=w.eps)
+    stream = torch.cuda.current_stream()
+    for t in range(Wu):
+        plan.step(Wd, grad_sets[t], hp, stream=stream)
+    torch.cuda.synchronize()
+    print("[bench] warmup done", file=sys.stderr, flush=True)
+
+    plan.profile_read(reset=True)
+    plan.profile_enable(True)
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    start.record(stream)
+    for t in range(K):
+        plan.step(Wd, grad_sets[Wu + t], hp, stream=stream)
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = start.elapsed_time(end)
+    prof = plan.profile_read(reset=True)
+    plan.profile_enable(False)
+    ms_per_step = total_ms / K
+    print(f"[bench] {ms_per_step:.3f} ms/step (wall {wall * 1e3 / K:.3f})", file=sys.stderr, flush=True)
+
+    # Per-kernel figures (ms per step, achieved rate, fraction of the bound).
+    kernels = {}
+    for name, v in prof.items():
+        if v["launches"] == 0:
+            continue
+        ms = v["ms"] / K
+        ent = {"ms_per_step": round(ms, 4), "launches_per_step": v["launches"] // K,
+               "avg_launch_ms": round(v["ms"] / v["launches"], 5)}
+        if v["bytes"] > 0 and ms > 0:
+            gbs = v["bytes"] / (ms * 1e-3) / 1e9
+            ent.update({"bound": "hbm", "GB_per_s": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4),
+                        "bytes_per_step": v["bytes"]})
+        if v["flops"] > 0 and ms > 0:
+            tf = v["flops"] / (ms * 1e-3) / 1e12
+            ent.update({"bound": "mfma", "TFLOP_per_s": round(tf, 1), "frac": round(tf / PEAK_BF16_TFLOPS, 4),
+                        "flops_per_step": v["flops"]})
+        kernels[name] = ent
+    ns = [prof[k] for k in ("ns_gram", "ns_poly", "ns_update")]
+    ns_ms = sum(v["ms"] for v in ns)
+    ns_launches = sum(v["launches"] for v in ns)
+    ns_flops_step = sum(v["flops"] for v in ns)
+    flops_per_launch = ns_flops_step * K / ns_launches
+    avg_launch_s = ns_ms * 1e-3 / ns_launches
+    achieved = flops_per_launch / avg_launch_s / 1e12
+    roofline = {"bound": "mfma", "kernel": "ns_gemm_kernel (Gram, polynomial and update phases)",
+                "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "flops_per_launch": flops_per_launch, "avg_launch_ms": round(avg_launch_s * 1e3, 4),
+                "flops_basis": "symmetric minimum: m'^2 n' (Gram) + m'^3 (A^2) + 2 m'^2 n' (B X) per NS iteration"}
+    ew_bytes = sum(prof[k]["bytes"] for k in ("momentum_rowcol", "scale_convert", "backmap_write"))
+    ew_ms = sum(prof[k]["ms"] for k in ("momentum_rowcol", "scale_convert", "backmap_write")) / K
+    hbm = {"elementwise_GB_per_s": round(ew_bytes / (ew_ms * 1e-3) / 1e9, 1),
+           "elementwise_frac": round(ew_bytes / (ew_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+
+    plan.close()
+    del grad_sets, Wd
+    torch.cuda.empty_cache()
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(w, args.cpu_sample_layers)
+
+    line = {"metric": METRIC, "value": round(ms_per_step, 4), "unit": "ms", "n_gpus": 1, "steps": K,
+            "warmup": Wu, "ms_per_step": round(ms_per_step, 4), "higher_is_better": False,
+            "scaling": "weak", "vs_baseline": None, "dtype": "bf16+fp32", "data": "synthetic",
+            "config": {"workload": w.name, "variant": w.variant, "matrices": len(shapes), "params": w.numel,
+                       "lr": w.lr, "grad_dist": w.dist, "timed": f"{K} consecutive steps, persistent state"},
+            "roofline": roofline, "hbm": hbm, "kernels": kernels, "cpu_baseline": cpu}
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

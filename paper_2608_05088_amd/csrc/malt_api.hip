@@ -1,0 +1,610 @@
+// Host runtime of libmalt: argument validation, the per-plan layout of the
+// caller's state and workspace buffers, grouped work lists, and the launch
+// sequence of one MALT / MALTER step (Algorithms 1 and 2).
+#include <math.h>
+#include <stdarg.h>
+#include <stddef.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <string>
+#include <vector>
+
+#include "../../include/libmalt.h"
+#include "malt_internal.h"
+
+using namespace malt;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+malt_status_t fail(malt_status_t st, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+malt_status_t fail(malt_status_t st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+malt_status_t hip_fail(hipError_t e, const char* what) {
+  return fail(MALT_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr int64_t kMaxDim = int64_t(1) << 20;        // rows or cols
+constexpr int64_t kMaxShort = 32768;                   // min(rows, cols): NS Gram side
+constexpr int64_t kMaxElems = (int64_t(1) << 31) - 1;  // rows * cols
+
+inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline int64_t pad_to(int64_t a, int64_t b) { return cdiv(a, b) * b; }
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct MatPlan {
+  int64_t m, n, mc, nc, mp, np;
+  bool tall, split;
+  int64_t k1_ct, k1_rt, k2_tr, k2_tc, k2_tiles, upd_tiles, sym_tiles;
+  // offsets
+  int64_t st_M, st_l, st_r, st_nu;     // floats from state base
+  size_t ws_scal, ws_Lv, ws_Rv, ws_rowpart, ws_colpart, ws_k2part, ws_gpart;
+  size_t ws_X[2], ws_XT[2], ws_A, ws_B;
+  // algorithmic cost
+  double ns_flops_sym_per_iter;        // 3 mc^2 nc + mc^3 (symmetric minimum)
+};
+
+struct Layout {
+  std::vector<MatPlan> mats;
+  size_t state_bytes = 0, ws_bytes = 0;
+  size_t ws_desc = 0, ws_ptrs = 0;
+  size_t ws_t_ew = 0, ws_t_fin = 0, ws_t_k2 = 0, ws_t_sym = 0, ws_t_upd = 0;
+  int64_t n_ew = 0, n_fin = 0, n_k2 = 0, n_sym = 0, n_upd = 0;
+};
+
+malt_status_t check_shapes(const malt_shape_t* shapes, int32_t n) {
+  if (n < 1) return fail(MALT_ERR_INVALID_ARG, "matrix count must be >= 1 (got %d)", n);
+  if (!shapes) return fail(MALT_ERR_INVALID_ARG, "shapes is NULL");
+  for (int32_t i = 0; i < n; ++i) {
+    const int64_t m = shapes[i].rows, c = shapes[i].cols;
+    if (m < 1 || c < 1) return fail(MALT_ERR_SHAPE, "matrix %d: rows/cols must be >= 1 (got %lld x %lld)",
+                                    i, (long long)m, (long long)c);
+    if (m > kMaxDim || c > kMaxDim || std::min(m, c) > kMaxShort || m * c > kMaxElems)
+      return fail(MALT_ERR_SHAPE, "matrix %d: %lld x %lld exceeds the supported size "
+                  "(dims <= 2^20, min dim <= 32768, elements < 2^31)", i, (long long)m, (long long)c);
+  }
+  return MALT_OK;
+}
+
+Layout make_layout(const malt_shape_t* shapes, int32_t n, malt_variant_t variant) {
+  Layout L;
+  L.mats.resize(n);
+  // State: [M... | l... | r... | nu...], float32, unpadded.
+  int64_t fo = 0;
+  for (int32_t i = 0; i < n; ++i) { L.mats[i].st_M = fo; fo += shapes[i].rows * shapes[i].cols; }
+  for (int32_t i = 0; i < n; ++i) { L.mats[i].st_l = fo; fo += shapes[i].rows; }
+  for (int32_t i = 0; i < n; ++i) { L.mats[i].st_r = fo; fo += shapes[i].cols; }
+  for (int32_t i = 0; i < n; ++i) {
+    if (variant == MALT_VARIANT_MALTER) { L.mats[i].st_nu = fo; fo += 1; } else { L.mats[i].st_nu = -1; }
+  }
+  L.state_bytes = size_t(fo) * 4;
+
+  for (int32_t i = 0; i < n; ++i) {
+    MatPlan& p = L.mats[i];
+    p.m = shapes[i].rows; p.n = shapes[i].cols;
+    p.tall = p.m > p.n;
+    p.mc = std::min(p.m, p.n); p.nc = std::max(p.m, p.n);
+    p.mp = pad_to(p.mc, NS_TILE); p.np = pad_to(p.nc, NS_TILE);
+    p.split = p.mc <= NS_SPLIT_MAX;
+    p.k1_ct = cdiv(p.n, EW_TC); p.k1_rt = cdiv(p.m, EW_TR);
+    const int64_t wrows_p = p.tall ? p.np : p.mp, wcols_p = p.tall ? p.mp : p.np;
+    p.k2_tr = wrows_p / K2_T; p.k2_tc = wcols_p / K2_T;
+    p.k2_tiles = p.k2_tr * p.k2_tc;
+    const int64_t T = p.mp / NS_TILE;
+    p.sym_tiles = T * (T + 1) / 2;
+    p.upd_tiles = T * (p.np / NS_TILE);
+    p.ns_flops_sym_per_iter = 3.0 * double(p.mc) * p.mc * p.nc + double(p.mc) * p.mc * p.mc;
+    L.n_ew += p.k1_rt * p.k1_ct;
+    L.n_fin += cdiv(p.m, NTHREADS) + cdiv(p.n, NTHREADS);
+    L.n_k2 += p.k2_tiles;
+    L.n_sym += p.sym_tiles;
+    L.n_upd += p.upd_tiles;
+  }
+  size_t off = 0;
+  auto take = [&](size_t bytes) { const size_t o = off; off = align256(off + bytes); return o; };
+  L.ws_desc = take(sizeof(MatDesc) * n);
+  L.ws_ptrs = take(sizeof(PtrPair) * n);
+  L.ws_t_ew = take(sizeof(Tile) * L.n_ew);
+  L.ws_t_fin = take(sizeof(Tile) * L.n_fin);
+  L.ws_t_k2 = take(sizeof(Tile) * L.n_k2);
+  L.ws_t_sym = take(sizeof(Tile) * L.n_sym);
+  L.ws_t_upd = take(sizeof(Tile) * L.n_upd);
+  for (int32_t i = 0; i < n; ++i) {
+    MatPlan& p = L.mats[i];
+    p.ws_scal = take(sizeof(double) * MAT_SCALARS);
+    p.ws_Lv = take(4 * p.m);
+    p.ws_Rv = take(4 * p.n);
+    p.ws_rowpart = take(4 * size_t(p.k1_ct) * p.m);
+    p.ws_colpart = take(4 * size_t(p.k1_rt) * p.n);
+    p.ws_k2part = take(8 * size_t(p.k2_tiles));
+    p.ws_gpart = take(8 * size_t(p.upd_tiles));
+    for (int b = 0; b < 2; ++b) p.ws_X[b] = take(2 * size_t(p.mp) * p.np);
+    for (int b = 0; b < 2; ++b) p.ws_XT[b] = take(2 * size_t(p.mp) * p.np);
+    p.ws_A = take(2 * size_t(p.mp) * p.mp);
+    p.ws_B = take(2 * size_t(p.mp) * p.mp * (p.split ? 2 : 1));
+  }
+  L.ws_bytes = off;
+  return L;
+}
+
+// Order of matrices in the grouped work lists: larger Newton-Schulz cost first.
+std::vector<int32_t> cost_order(const Layout& L) {
+  std::vector<int32_t> ord(L.mats.size());
+  for (size_t i = 0; i < ord.size(); ++i) ord[i] = int32_t(i);
+  std::stable_sort(ord.begin(), ord.end(), [&](int32_t a, int32_t b) {
+    return L.mats[a].ns_flops_sym_per_iter > L.mats[b].ns_flops_sym_per_iter;
+  });
+  return ord;
+}
+
+bool ranges_overlap(uintptr_t a0, size_t an, uintptr_t b0, size_t bn) {
+  return a0 < b0 + bn && b0 < a0 + an;
+}
+
+}  // namespace
+
+struct malt_plan {
+  Layout L;
+  malt_variant_t variant;
+  int32_t n = 0;
+  std::vector<malt_shape_t> shapes;
+  char* state = nullptr;
+  char* ws = nullptr;
+  int64_t t = 0;
+  // pointer table staging
+  PtrPair* h_ptrs = nullptr;          // pinned
+  std::vector<PtrPair> cur_ptrs;
+  bool ptrs_valid = false;
+  hipEvent_t ptr_ev = nullptr;
+  bool ptr_ev_recorded = false;
+  // profiling
+  bool prof = false;
+  struct EvSet { std::vector<hipEvent_t> ev; std::vector<int> phase; };
+  std::vector<EvSet> pending;
+  std::vector<hipEvent_t> free_events;
+  double prof_ms[MALT_NUM_PHASES] = {0};
+  int64_t prof_launches[MALT_NUM_PHASES] = {0};
+  int32_t last_ns_steps = 5;
+};
+
+namespace {
+
+hipEvent_t get_event(malt_plan* p) {
+  if (!p->free_events.empty()) {
+    hipEvent_t e = p->free_events.back();
+    p->free_events.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+hipError_t drain_profile(malt_plan* p) {
+  for (auto& s : p->pending) {
+    if (s.ev.empty()) continue;
+    hipError_t e = hipEventSynchronize(s.ev.back());
+    if (e != hipSuccess) return e;
+    for (size_t k = 1; k < s.ev.size(); ++k) {
+      float ms = 0.f;
+      e = hipEventElapsedTime(&ms, s.ev[k - 1], s.ev[k]);
+      if (e != hipSuccess) return e;
+      p->prof_ms[s.phase[k - 1]] += ms;
+      p->prof_launches[s.phase[k - 1]] += 1;
+    }
+    for (hipEvent_t ev : s.ev) p->free_events.push_back(ev);
+  }
+  p->pending.clear();
+  return hipSuccess;
+}
+
+malt_status_t check_hparams(const malt_hparams_t* hp) {
+  if (!hp) return fail(MALT_ERR_INVALID_ARG, "hparams is NULL");
+  if (!(hp->lr >= 0.0) || !isfinite(hp->lr)) return fail(MALT_ERR_INVALID_ARG, "lr must be finite and >= 0");
+  if (!(hp->mu1 >= 0.0 && hp->mu1 < 1.0)) return fail(MALT_ERR_INVALID_ARG, "mu1 must be in [0, 1)");
+  if (!(hp->mu2 >= 0.0 && hp->mu2 < 1.0)) return fail(MALT_ERR_INVALID_ARG, "mu2 must be in [0, 1)");
+  if (!(hp->eps > 0.0) || !isfinite(hp->eps)) return fail(MALT_ERR_INVALID_ARG, "eps must be finite and > 0");
+  if (!(hp->weight_decay >= 0.0) || !isfinite(hp->weight_decay))
+    return fail(MALT_ERR_INVALID_ARG, "weight_decay must be finite and >= 0");
+  if (hp->ns_steps < 1 || hp->ns_steps > 64) return fail(MALT_ERR_INVALID_ARG, "ns_steps must be in [1, 64]");
+  if (!isfinite(hp->ns_a) || !isfinite(hp->ns_b) || !isfinite(hp->ns_c))
+    return fail(MALT_ERR_INVALID_ARG, "Newton-Schulz coefficients must be finite");
+  if (!(hp->ns_eps >= 0.0) || !isfinite(hp->ns_eps)) return fail(MALT_ERR_INVALID_ARG, "ns_eps must be finite and >= 0");
+  return MALT_OK;
+}
+
+void fill_desc(const malt_plan* p, std::vector<MatDesc>& D) {
+  D.resize(p->n);
+  for (int32_t i = 0; i < p->n; ++i) {
+    const MatPlan& q = p->L.mats[i];
+    MatDesc& d = D[i];
+    memset(&d, 0, sizeof(d));
+    d.m = int32_t(q.m); d.n = int32_t(q.n);
+    d.mc = int32_t(q.mc); d.nc = int32_t(q.nc);
+    d.mp = int32_t(q.mp); d.np = int32_t(q.np);
+    d.tall = q.tall ? 1 : 0;
+    d.split = q.split ? 1 : 0;
+    d.k1_ct = int32_t(q.k1_ct); d.k1_rt = int32_t(q.k1_rt);
+    d.k2_tiles = int32_t(q.k2_tiles); d.upd_tiles = int32_t(q.upd_tiles);
+    float* st = reinterpret_cast<float*>(p->state);
+    d.M = st + q.st_M; d.l = st + q.st_l; d.r = st + q.st_r;
+    d.nu = q.st_nu >= 0 ? st + q.st_nu : nullptr;
+    char* w = p->ws;
+    d.Lv = reinterpret_cast<float*>(w + q.ws_Lv);
+    d.Rv = reinterpret_cast<float*>(w + q.ws_Rv);
+    d.rowpart = reinterpret_cast<float*>(w + q.ws_rowpart);
+    d.colpart = reinterpret_cast<float*>(w + q.ws_colpart);
+    d.k2part = reinterpret_cast<float*>(w + q.ws_k2part);
+    d.gpart = reinterpret_cast<float*>(w + q.ws_gpart);
+    for (int b = 0; b < 2; ++b) {
+      d.X[b] = reinterpret_cast<bf16_t*>(w + q.ws_X[b]);
+      d.XT[b] = reinterpret_cast<bf16_t*>(w + q.ws_XT[b]);
+    }
+    d.A = reinterpret_cast<bf16_t*>(w + q.ws_A);
+    d.B = reinterpret_cast<bf16_t*>(w + q.ws_B);
+    d.scal = reinterpret_cast<double*>(w + q.ws_scal);
+  }
+}
+
+void build_tiles(const malt_plan* p, std::vector<Tile>& ew, std::vector<Tile>& fin, std::vector<Tile>& k2,
+                 std::vector<Tile>& sym, std::vector<Tile>& upd) {
+  const std::vector<int32_t> ord = cost_order(p->L);
+  for (int32_t i : ord) {
+    const MatPlan& q = p->L.mats[i];
+    for (int32_t ti = 0; ti < q.k1_rt; ++ti)
+      for (int32_t tj = 0; tj < q.k1_ct; ++tj) ew.push_back({i, ti, tj, 0});
+    for (int32_t c = 0; c < cdiv(q.m, NTHREADS); ++c) fin.push_back({i, 0, c, 0});
+    for (int32_t c = 0; c < cdiv(q.n, NTHREADS); ++c) fin.push_back({i, 1, c, 0});
+    int32_t idx = 0;
+    for (int32_t ti = 0; ti < q.k2_tr; ++ti)
+      for (int32_t tj = 0; tj < q.k2_tc; ++tj) k2.push_back({i, ti, tj, idx++});
+    const int32_t T = int32_t(q.mp / NS_TILE), TN = int32_t(q.np / NS_TILE);
+    idx = 0;
+    for (int32_t ti = 0; ti < T; ++ti)
+      for (int32_t tj = ti; tj < T; ++tj) sym.push_back({i, ti, tj, idx++});
+    idx = 0;
+    for (int32_t tj = 0; tj < TN; ++tj)       // column panel major: neighbours share X^T panels
+      for (int32_t ti = 0; ti < T; ++ti) upd.push_back({i, ti, tj, idx++});
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+void malt_hparams_default(malt_hparams_t* hp) {
+  if (!hp) return;
+  hp->lr = 1.3e-3;
+  hp->mu1 = 0.95;
+  hp->mu2 = 0.99;
+  hp->eps = 1e-8;
+  hp->weight_decay = 0.0;
+  hp->ns_steps = 5;
+  hp->ns_a = 3.4445;
+  hp->ns_b = -4.7750;
+  hp->ns_c = 2.0315;
+  hp->ns_eps = 1e-7;
+  hp->precond_identity = 0;
+}
+
+malt_status_t malt_state_size(const malt_shape_t* shapes, int32_t n, malt_variant_t variant,
+                              size_t* state_bytes, size_t* workspace_bytes) {
+  if (variant != MALT_VARIANT_MALT && variant != MALT_VARIANT_MALTER)
+    return fail(MALT_ERR_INVALID_ARG, "unknown variant %d", int(variant));
+  if (!state_bytes || !workspace_bytes) return fail(MALT_ERR_INVALID_ARG, "output pointer is NULL");
+  malt_status_t st = check_shapes(shapes, n);
+  if (st != MALT_OK) return st;
+  const Layout L = make_layout(shapes, n, variant);
+  *state_bytes = L.state_bytes;
+  *workspace_bytes = L.ws_bytes;
+  return MALT_OK;
+}
+
+malt_status_t malt_init_state(malt_plan_t** out, const malt_shape_t* shapes, int32_t n,
+                              malt_variant_t variant, void* state_mem, void* workspace_mem,
+                              int32_t from_existing, int64_t step, void* stream) {
+  if (!out) return fail(MALT_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (variant != MALT_VARIANT_MALT && variant != MALT_VARIANT_MALTER)
+    return fail(MALT_ERR_INVALID_ARG, "unknown variant %d", int(variant));
+  malt_status_t st = check_shapes(shapes, n);
+  if (st != MALT_OK) return st;
+  if (!state_mem || !workspace_mem) return fail(MALT_ERR_INVALID_ARG, "state or workspace pointer is NULL");
+  if (reinterpret_cast<uintptr_t>(state_mem) % 16 != 0)
+    return fail(MALT_ERR_ALIGNMENT, "state_mem must be 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(workspace_mem) % 256 != 0)
+    return fail(MALT_ERR_ALIGNMENT, "workspace_mem must be 256-byte aligned");
+  if (from_existing != 0 && from_existing != 1) return fail(MALT_ERR_INVALID_ARG, "from_existing must be 0 or 1");
+  if (from_existing && step < 0) return fail(MALT_ERR_INVALID_ARG, "step must be >= 0");
+
+  malt_plan* p = new malt_plan();
+  p->L = make_layout(shapes, n, variant);
+  if (ranges_overlap(reinterpret_cast<uintptr_t>(state_mem), p->L.state_bytes,
+                     reinterpret_cast<uintptr_t>(workspace_mem), p->L.ws_bytes)) {
+    delete p;
+    return fail(MALT_ERR_ALIAS, "state and workspace buffers overlap");
+  }
+  p->variant = variant;
+  p->n = n;
+  p->shapes.assign(shapes, shapes + n);
+  p->state = static_cast<char*>(state_mem);
+  p->ws = static_cast<char*>(workspace_mem);
+  p->t = from_existing ? step : 0;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  std::vector<MatDesc> D;
+  fill_desc(p, D);
+  std::vector<Tile> ew, fin, k2, sym, upd;
+  build_tiles(p, ew, fin, k2, sym, upd);
+
+  // Stage every table in one pinned buffer laid out like the workspace head.
+  const size_t head = p->L.ws_t_upd + sizeof(Tile) * upd.size();
+  void* h = nullptr;
+  hipError_t e = hipHostMalloc(&h, head, hipHostMallocDefault);
+  if (e != hipSuccess) { delete p; return hip_fail(e, "hipHostMalloc"); }
+  memset(h, 0, head);
+  char* hc = static_cast<char*>(h);
+  memcpy(hc + p->L.ws_desc, D.data(), sizeof(MatDesc) * n);
+  memcpy(hc + p->L.ws_t_ew, ew.data(), sizeof(Tile) * ew.size());
+  memcpy(hc + p->L.ws_t_fin, fin.data(), sizeof(Tile) * fin.size());
+  memcpy(hc + p->L.ws_t_k2, k2.data(), sizeof(Tile) * k2.size());
+  memcpy(hc + p->L.ws_t_sym, sym.data(), sizeof(Tile) * sym.size());
+  memcpy(hc + p->L.ws_t_upd, upd.data(), sizeof(Tile) * upd.size());
+
+  e = hipMemsetAsync(p->ws, 0, p->L.ws_bytes, s);
+  if (e == hipSuccess) e = hipMemcpyAsync(p->ws, hc, head, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess && !from_existing) e = hipMemsetAsync(p->state, 0, p->L.state_bytes, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  (void)hipHostFree(h);
+  if (e != hipSuccess) { delete p; return hip_fail(e, "uploading plan tables"); }
+
+  e = hipHostMalloc(reinterpret_cast<void**>(&p->h_ptrs), sizeof(PtrPair) * n, hipHostMallocDefault);
+  if (e != hipSuccess) { delete p; return hip_fail(e, "hipHostMalloc"); }
+  e = hipEventCreateWithFlags(&p->ptr_ev, hipEventDisableTiming);
+  if (e != hipSuccess) { (void)hipHostFree(p->h_ptrs); delete p; return hip_fail(e, "hipEventCreate"); }
+  p->cur_ptrs.assign(n, PtrPair{nullptr, nullptr, 0, 0});
+  *out = p;
+  return MALT_OK;
+}
+
+malt_status_t malt_step(malt_plan_t* p, float* const* params, const float* const* grads,
+                        const malt_shape_t* shapes, int32_t n, const malt_hparams_t* hp, void* stream) {
+  if (!p) return fail(MALT_ERR_INVALID_ARG, "plan is NULL");
+  if (!params || !grads) return fail(MALT_ERR_INVALID_ARG, "params or grads is NULL");
+  malt_status_t st = check_hparams(hp);
+  if (st != MALT_OK) return st;
+  if (n != p->n || !shapes) return fail(MALT_ERR_STATE_MISMATCH, "matrix count %d differs from the plan's %d", n, p->n);
+  for (int32_t i = 0; i < n; ++i)
+    if (shapes[i].rows != p->shapes[i].rows || shapes[i].cols != p->shapes[i].cols)
+      return fail(MALT_ERR_STATE_MISMATCH, "matrix %d: shape %lld x %lld differs from the plan's %lld x %lld", i,
+                  (long long)shapes[i].rows, (long long)shapes[i].cols, (long long)p->shapes[i].rows,
+                  (long long)p->shapes[i].cols);
+  // Pointer checks (host-side, before any enqueue).
+  bool changed = !p->ptrs_valid;
+  const uintptr_t s0 = reinterpret_cast<uintptr_t>(p->state), w0 = reinterpret_cast<uintptr_t>(p->ws);
+  for (int32_t i = 0; i < n; ++i) {
+    const uintptr_t W = reinterpret_cast<uintptr_t>(params[i]), G = reinterpret_cast<uintptr_t>(grads[i]);
+    if (!W || !G) return fail(MALT_ERR_INVALID_ARG, "matrix %d: NULL param or grad", i);
+    if (W % 4 || G % 4) return fail(MALT_ERR_ALIGNMENT, "matrix %d: param/grad not 4-byte aligned", i);
+    const size_t bytes = size_t(p->shapes[i].rows) * p->shapes[i].cols * 4;
+    if (ranges_overlap(W, bytes, G, bytes)) return fail(MALT_ERR_ALIAS, "matrix %d: param and grad overlap", i);
+    if (ranges_overlap(W, bytes, s0, p->L.state_bytes) || ranges_overlap(G, bytes, s0, p->L.state_bytes) ||
+        ranges_overlap(W, bytes, w0, p->L.ws_bytes) || ranges_overlap(G, bytes, w0, p->L.ws_bytes))
+      return fail(MALT_ERR_ALIAS, "matrix %d: param/grad overlaps the state or workspace", i);
+    if (p->cur_ptrs[i].W != params[i] || p->cur_ptrs[i].G != grads[i]) changed = true;
+  }
+  if (changed && n > 1) {
+    // Parameters are updated in place: they must not overlap one another.
+    std::vector<std::pair<uintptr_t, size_t>> rs(n);
+    for (int32_t i = 0; i < n; ++i)
+      rs[i] = {reinterpret_cast<uintptr_t>(params[i]), size_t(p->shapes[i].rows) * p->shapes[i].cols * 4};
+    std::sort(rs.begin(), rs.end());
+    for (int32_t i = 1; i < n; ++i)
+      if (rs[i - 1].first + rs[i - 1].second > rs[i].first)
+        return fail(MALT_ERR_ALIAS, "two parameter matrices overlap");
+  }
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e;
+  if (changed) {
+    if (p->ptr_ev_recorded) {
+      e = hipEventSynchronize(p->ptr_ev);   // previous upload has left the staging buffer
+      if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+    }
+    for (int32_t i = 0; i < n; ++i) {
+      // The vectorised elementwise path needs 16-byte aligned rows of W, G and M.
+      const MatPlan& q = p->L.mats[i];
+      const uintptr_t M = reinterpret_cast<uintptr_t>(p->state) + 4 * size_t(q.st_M);
+      p->h_ptrs[i].W = params[i];
+      p->h_ptrs[i].G = grads[i];
+      p->h_ptrs[i].vec = (q.n % 4 == 0) && (reinterpret_cast<uintptr_t>(params[i]) % 16 == 0) &&
+                         (reinterpret_cast<uintptr_t>(grads[i]) % 16 == 0) && (M % 16 == 0);
+      p->h_ptrs[i].pad_ = 0;
+      p->cur_ptrs[i] = p->h_ptrs[i];
+    }
+    e = hipMemcpyAsync(p->ws + p->L.ws_ptrs, p->h_ptrs, sizeof(PtrPair) * n, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipEventRecord(p->ptr_ev, s);
+    if (e != hipSuccess) { p->ptrs_valid = false; return hip_fail(e, "uploading pointer table"); }
+    p->ptr_ev_recorded = true;
+    p->ptrs_valid = true;
+  }
+
+  const int64_t t = p->t + 1;
+  EwArgs ea;
+  ea.desc = reinterpret_cast<const MatDesc*>(p->ws + p->L.ws_desc);
+  ea.ptrs = reinterpret_cast<const PtrPair*>(p->ws + p->L.ws_ptrs);
+  ea.tiles = nullptr;
+  ea.ntiles = 0;
+  ea.mu1 = float(hp->mu1);
+  ea.one_minus_mu1 = float(1.0 - hp->mu1);
+  ea.mu2 = hp->mu2;
+  ea.eps = hp->eps;
+  ea.bc = sqrt(1.0 - pow(hp->mu2, double(t))) / (1.0 - pow(hp->mu1, double(t)) + hp->eps);
+  ea.ns_eps = hp->ns_eps;
+  ea.lr = hp->lr;
+  ea.decay = float(1.0 - hp->lr * hp->weight_decay);
+  ea.malter = p->variant == MALT_VARIANT_MALTER;
+  ea.identity = hp->precond_identity != 0;
+  ea.o_parity = hp->ns_steps & 1;
+
+  malt_plan::EvSet evs;
+  auto mark = [&](int phase) -> hipError_t {
+    if (!p->prof) return hipSuccess;
+    hipEvent_t ev = get_event(p);
+    if (!ev) return hipErrorOutOfMemory;
+    evs.ev.push_back(ev);
+    evs.phase.push_back(phase);
+    return hipEventRecord(ev, s);
+  };
+  auto tiles_at = [&](size_t off) { return reinterpret_cast<const Tile*>(p->ws + off); };
+
+#define MALT_LAUNCH(phase, call)                            \
+  do {                                                      \
+    if ((e = mark(phase)) != hipSuccess) goto hip_error;    \
+    if ((e = (call)) != hipSuccess) goto hip_error;         \
+  } while (0)
+  {
+    ea.tiles = tiles_at(p->L.ws_t_ew); ea.ntiles = int32_t(p->L.n_ew);
+    MALT_LAUNCH(0, launch_momentum_rowcol(ea, s));
+    ea.tiles = tiles_at(p->L.ws_t_fin); ea.ntiles = int32_t(p->L.n_fin);
+    MALT_LAUNCH(1, launch_precond_finalize(ea, s));
+    ea.tiles = tiles_at(p->L.ws_t_k2); ea.ntiles = int32_t(p->L.n_k2);
+    MALT_LAUNCH(2, launch_scale_convert(ea, s));
+    MALT_LAUNCH(3, launch_norm_scalars(ea, n, s));
+    NsArgs na;
+    na.desc = ea.desc;
+    na.a = float(hp->ns_a); na.b = float(hp->ns_b); na.c = float(hp->ns_c);
+    for (int32_t it = 0; it < hp->ns_steps; ++it) {
+      na.first = it == 0;
+      na.last = it == hp->ns_steps - 1;
+      na.src = it & 1;
+      na.tiles = tiles_at(p->L.ws_t_sym); na.ntiles = int32_t(p->L.n_sym);
+      na.phase = PH_GRAM;
+      MALT_LAUNCH(4, launch_ns_gemm(na, s));
+      na.phase = PH_POLY;
+      MALT_LAUNCH(5, launch_ns_gemm(na, s));
+      na.tiles = tiles_at(p->L.ws_t_upd); na.ntiles = int32_t(p->L.n_upd);
+      na.phase = PH_UPDATE;
+      MALT_LAUNCH(6, launch_ns_gemm(na, s));
+    }
+    MALT_LAUNCH(7, launch_graft_scalars(ea, n, s));
+    ea.tiles = tiles_at(p->L.ws_t_ew); ea.ntiles = int32_t(p->L.n_ew);
+    MALT_LAUNCH(8, launch_backmap_write(ea, s));
+    if ((e = mark(-1)) != hipSuccess) goto hip_error;
+  }
+#undef MALT_LAUNCH
+  if (p->prof) {
+    p->pending.push_back(std::move(evs));
+    if (p->pending.size() > 256) {
+      e = drain_profile(p);
+      if (e != hipSuccess) return hip_fail(e, "reading profile events");
+    }
+  }
+  p->last_ns_steps = hp->ns_steps;
+  p->t = t;
+  return MALT_OK;
+hip_error:
+  for (hipEvent_t ev : evs.ev) p->free_events.push_back(ev);
+  return hip_fail(e, "launching step kernels");
+}
+
+malt_status_t malt_state_layout(const malt_plan_t* p, int32_t i, malt_state_layout_t* out) {
+  if (!p || !out) return fail(MALT_ERR_INVALID_ARG, "NULL argument");
+  if (i < 0 || i >= p->n) return fail(MALT_ERR_INVALID_ARG, "matrix index %d out of range", i);
+  const MatPlan& q = p->L.mats[i];
+  out->M = q.st_M; out->l = q.st_l; out->r = q.st_r; out->nu = q.st_nu;
+  return MALT_OK;
+}
+
+malt_status_t malt_debug_layout(const malt_plan_t* p, int32_t i, malt_debug_layout_t* out) {
+  if (!p || !out) return fail(MALT_ERR_INVALID_ARG, "NULL argument");
+  if (i < 0 || i >= p->n) return fail(MALT_ERR_INVALID_ARG, "matrix index %d out of range", i);
+  const MatPlan& q = p->L.mats[i];
+  const int par = p->last_ns_steps & 1;
+  out->Lv = int64_t(q.ws_Lv);
+  out->Rv = int64_t(q.ws_Rv);
+  out->O = int64_t(q.tall ? q.ws_XT[par] : q.ws_X[par]);
+  out->X0 = int64_t(q.tall ? q.ws_XT[0] : q.ws_X[0]);
+  out->O_pitch = q.tall ? q.mp : q.np;
+  out->scalars = int64_t(q.ws_scal);
+  return MALT_OK;
+}
+
+int64_t malt_plan_step(const malt_plan_t* p) { return p ? p->t : -1; }
+
+malt_status_t malt_profile_enable(malt_plan_t* p, int32_t enable) {
+  if (!p) return fail(MALT_ERR_INVALID_ARG, "plan is NULL");
+  p->prof = enable != 0;
+  return MALT_OK;
+}
+
+malt_status_t malt_profile_read(malt_plan_t* p, malt_profile_t* out, int32_t reset) {
+  if (!p || !out) return fail(MALT_ERR_INVALID_ARG, "NULL argument");
+  hipError_t e = drain_profile(p);
+  if (e != hipSuccess) return hip_fail(e, "reading profile events");
+  memset(out, 0, sizeof(*out));
+  for (int k = 0; k < MALT_NUM_PHASES; ++k) {
+    out->ms[k] = p->prof_ms[k];
+    out->launches[k] = p->prof_launches[k];
+  }
+  // Algorithmic bytes / flops of one step (float32 = 4 B, bf16 = 2 B).
+  const bool malter = p->variant == MALT_VARIANT_MALTER;
+  for (const MatPlan& q : p->L.mats) {
+    const double el = double(q.m) * q.n, mn = double(q.m + q.n);
+    out->bytes[0] += 12.0 * el + 4.0 * mn;                      // G, M in; M out; row/col partials
+    out->bytes[1] += 8.0 * mn + 4.0 * mn;                       // l, r in/out, L, R out
+    out->bytes[2] += (malter ? 8.0 : 4.0) * el + 4.0 * el;      // M (+G) in; X0 in two orientations
+    out->bytes[8] += 10.0 * el;                                 // W, O in; W out
+    const int steps = p->last_ns_steps;
+    out->flops[4] += steps * double(q.mc) * q.mc * q.nc;            // X X^T, one triangle
+    out->flops[5] += steps * double(q.mc) * q.mc * q.mc;            // A A, one triangle
+    out->flops[6] += steps * 2.0 * double(q.mc) * q.mc * q.nc;      // B X (once, also when split)
+  }
+  if (reset) {
+    memset(p->prof_ms, 0, sizeof(p->prof_ms));
+    memset(p->prof_launches, 0, sizeof(p->prof_launches));
+  }
+  return MALT_OK;
+}
+
+void malt_destroy_state(malt_plan_t* p) {
+  if (!p) return;
+  (void)drain_profile(p);
+  for (hipEvent_t ev : p->free_events) (void)hipEventDestroy(ev);
+  if (p->ptr_ev) {
+    if (p->ptr_ev_recorded) (void)hipEventSynchronize(p->ptr_ev);
+    (void)hipEventDestroy(p->ptr_ev);
+  }
+  if (p->h_ptrs) (void)hipHostFree(p->h_ptrs);
+  delete p;
+}
+
+const char* malt_status_string(malt_status_t s) {
+  switch (s) {
+    case MALT_OK: return "MALT_OK";
+    case MALT_ERR_INVALID_ARG: return "MALT_ERR_INVALID_ARG";
+    case MALT_ERR_SHAPE: return "MALT_ERR_SHAPE";
+    case MALT_ERR_ALIGNMENT: return "MALT_ERR_ALIGNMENT";
+    case MALT_ERR_STATE_MISMATCH: return "MALT_ERR_STATE_MISMATCH";
+    case MALT_ERR_HIP: return "MALT_ERR_HIP";
+    case MALT_ERR_ALIAS: return "MALT_ERR_ALIAS";
+  }
+  return "MALT_ERR_UNKNOWN";
+}
+
+const char* malt_last_error(void) { return g_last_error.c_str(); }
+
+const char* malt_version(void) { return "libmalt 0.1 (gfx950)"; }
+
+}  // extern "C"

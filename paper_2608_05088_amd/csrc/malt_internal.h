@@ -1,0 +1,132 @@
+// Internal device-side structures and kernel launchers of libmalt (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace malt {
+
+// Elementwise tiles (momentum / back-map): EW_TR rows x EW_TC cols per
+// 256-thread workgroup; each lane owns 4 consecutive columns.
+constexpr int EW_TR = 32;
+constexpr int EW_TC = 256;
+// Scale+convert tile (with an LDS transpose): K2_T x K2_T.
+constexpr int K2_T = 64;
+// Newton-Schulz output tile and padding unit of the bf16 buffers.
+constexpr int NS_TILE = 256;
+constexpr int NS_BK = 64;
+// Matrices whose short side is at most this carry B = b A + c A^2 as a bf16
+// pair (hi, lo = bf16(B - hi)) into the update product: with few singular
+// values the rounding of the small m' x m' polynomial is not averaged away.
+constexpr int NS_SPLIT_MAX = 128;
+// Threads of every workgroup.
+constexpr int NTHREADS = 256;
+
+typedef uint16_t bf16_t;   // bf16 storage
+
+// Per-matrix scalar slots (float64) in the workspace.
+enum {
+  SC_S = 0,       // ||L M R||_F
+  SC_SIGMA = 1,   // 1 / (s + ns_eps)
+  SC_NU = 2,      // nu_t (MALTER)
+  SC_ALPHA = 3,   // alpha_t (1 for MALT)
+  SC_O2 = 4,      // ||O||_F^2
+  SC_D2 = 5,      // ||L O R||_F^2
+  SC_GRAFT = 6,   // ||O|| / (||D|| + eps)
+  SC_COEF = 7,    // lr * alpha * graft
+  SC_Q = 8,       // ||L G R||_F^2 (MALTER)
+  MAT_SCALARS = 16
+};
+
+struct MatDesc {
+  int32_t m, n;        // W rows, cols
+  int32_t mc, nc;      // canonical orientation: mc = min(m,n) rows, nc = max(m,n) cols
+  int32_t mp, np;      // canonical dims padded to NS_TILE
+  int32_t tall;        // 1 when m > n: canonical = W^T
+  int32_t split;       // 1: B stored as [hi | lo] (row pitch 2*mp)
+  int32_t k1_ct;       // column tiles of the momentum pass (row partial count)
+  int32_t k1_rt;       // row tiles of the momentum pass (column partial count)
+  int32_t k2_tiles;    // scale+convert tiles (norm partial count)
+  int32_t upd_tiles;   // NS update tiles (graft partial count)
+  float* M;
+  float* l;
+  float* r;
+  float* nu;           // nullptr for MALT
+  float* Lv;           // m
+  float* Rv;           // n
+  float* rowpart;      // [k1_ct][m]
+  float* colpart;      // [k1_rt][n]
+  float* k2part;       // [k2_tiles][2]: sum (LMR)^2, sum (LGR)^2
+  float* gpart;        // [upd_tiles][2]: sum O^2, sum (LOR)^2
+  bf16_t* X[2];        // canonical mp x np, row-major
+  bf16_t* XT[2];       // canonical transpose np x mp, row-major
+  bf16_t* A;           // mp x mp  (Gram / A)
+  bf16_t* B;           // mp x mp, or mp x 2mp [hi | lo] when split (b A + c A^2)
+  double* scal;        // MAT_SCALARS
+};
+
+// Per-step caller pointers; vec = 1 when W, G and M rows allow 16-byte access.
+struct PtrPair {
+  float* W;
+  const float* G;
+  int32_t vec;
+  int32_t pad_;
+};
+
+// One unit of work of a grouped launch.
+//   momentum/back-map: (mat, row tile, col tile, -)
+//   preconditioner finalise: (mat, 0 = rows | 1 = cols, chunk, -)
+//   scale+convert: (mat, row tile, col tile, partial slot)
+//   NS: (mat, tile row, tile col, partial slot)
+struct Tile {
+  int32_t mat, ti, tj, idx;
+};
+
+enum { PH_GRAM = 0, PH_POLY = 1, PH_UPDATE = 2 };
+
+struct EwArgs {
+  const MatDesc* desc;
+  const PtrPair* ptrs;
+  const Tile* tiles;
+  int32_t ntiles;
+  float mu1, one_minus_mu1;
+  double mu2, eps;
+  double bc;             // sqrt(1 - mu2^t) / (1 - mu1^t + eps)
+  double ns_eps;
+  double lr;
+  float decay;           // 1 - lr * weight_decay
+  int32_t malter;
+  int32_t identity;
+  int32_t o_parity;      // which X/XT buffer holds the final O
+};
+
+struct NsArgs {
+  const MatDesc* desc;
+  const Tile* tiles;
+  int32_t ntiles;
+  int32_t phase;
+  int32_t first;         // iteration 0: apply sigma
+  int32_t last;          // final iteration: write O and graft partials
+  int32_t src;           // X[src] / XT[src] is the current iterate
+  float a, b, c;
+};
+
+// Launchers (stream-ordered, no synchronisation).
+hipError_t launch_momentum_rowcol(const EwArgs& a, hipStream_t s);
+hipError_t launch_precond_finalize(const EwArgs& a, hipStream_t s);
+hipError_t launch_scale_convert(const EwArgs& a, hipStream_t s);
+hipError_t launch_norm_scalars(const EwArgs& a, int32_t nmat, hipStream_t s);
+hipError_t launch_graft_scalars(const EwArgs& a, int32_t nmat, hipStream_t s);
+hipError_t launch_backmap_write(const EwArgs& a, hipStream_t s);
+hipError_t launch_ns_gemm(const NsArgs& a, hipStream_t s);
+
+// Map a workgroup id to a work index so that the workgroups that land on one
+// XCD (dispatched round-robin over 8 XCDs) take a contiguous run of the work
+// list; a bijection on [0, n).
+__device__ __forceinline__ int xcd_remap(int b, int n) {
+  const int q = n >> 3, r = n & 7;
+  const int x = b & 7, k = b >> 3;
+  return (x < r) ? x * (q + 1) + k : r * (q + 1) + (x - r) * q + k;
+}
+
+}  // namespace malt

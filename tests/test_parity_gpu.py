@@ -1,0 +1,188 @@
+"""GPU parity of libmalt against the fp64 oracle, through the C ABI.
+
+Inputs are the seeded synthetic workloads; the HIP path and the oracle get the
+same float32 buffers.  Each test prints its case before touching the GPU.
+"""
+import numpy as np
+import pytest
+
+from gpu_harness import TOL_NS, TOL_STATE, compare, run_gpu, run_oracle, say, to_dev
+from oracle import rel_fro
+from paper_2608_05088_amd import libmalt as lm
+from paper_2608_05088_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    lm.lib()   # raises if the library is not built: no fallback
+
+
+def _hp(w: wl.Workload, **kw):
+    d = dict(lr=w.lr, mu1=w.mu1, mu2=w.mu2, eps=w.eps)
+    d.update(kw)
+    return d
+
+
+def _inputs(w: wl.Workload, steps: int, indices=None, cid=None):
+    cid = w.cid if cid is None else cid
+    idx = list(range(len(w.shapes))) if indices is None else list(indices)
+    W0 = [wl.weight(cid, i, w.shapes[i]) for i in idx]
+    grads = [[wl.grad(cid, t, i, w.shapes[i], w.dist) for i in idx] for t in range(1, steps + 1)]
+    return W0, grads
+
+
+def test_c1_single_matrix_three_steps():
+    w = wl.WORKLOADS[1]
+    say(f"[parity] C1 {w.shapes} malt x{w.steps}")
+    W0, grads = _inputs(w, w.steps)
+    g = run_gpu(list(w.shapes), w.variant, W0, grads, _hp(w))
+    o = run_oracle(list(w.shapes), w.variant, W0, grads, _hp(w))
+    worst = compare(g, o, w.variant, label="C1")
+    say(f"[parity] C1 worst {worst}")
+
+
+RAGGED = [(300, 200), (1, 257), (257, 1), (129, 513), (64, 64), (3, 1000), (513, 129), (1, 1), (250, 250)]
+
+
+@pytest.mark.parametrize("variant", ["malt", "malter"])
+def test_ragged_shapes_multi_step(variant):
+    say(f"[parity] ragged {RAGGED} {variant} x3")
+    rng_shapes = RAGGED
+    W0 = [wl.weight(90, i, s) for i, s in enumerate(rng_shapes)]
+    grads = [[wl.grad(90, t, i, s, "row_loguniform") for i, s in enumerate(rng_shapes)] for t in (1, 2, 3)]
+    hp = dict(lr=3e-3)
+    g = run_gpu(rng_shapes, variant, W0, grads, hp)
+    o = run_oracle(rng_shapes, variant, W0, grads, hp)
+    worst = compare(g, o, variant, label="ragged")
+    say(f"[parity] ragged worst {worst}")
+
+
+def test_unaligned_pointers_take_scalar_path():
+    # Params/grads offset by one float inside larger buffers: 4-byte aligned only.
+    import torch
+    shapes = [(64, 128), (96, 64)]
+    say(f"[parity] unaligned {shapes}")
+    W0 = [wl.weight(91, i, s) for i, s in enumerate(shapes)]
+    grads = [[wl.grad(91, t, i, s) for i, s in enumerate(shapes)] for t in (1, 2)]
+    hp = dict(lr=1e-2)
+    plan = lm.Plan(shapes, "malt")
+    bufW = [torch.zeros(m * n + 1, device="cuda") for m, n in shapes]
+    bufG = [torch.zeros(m * n + 1, device="cuda") for m, n in shapes]
+    Wd = [b[1:].view(s) for b, s in zip(bufW, shapes)]
+    for wd, w0 in zip(Wd, W0):
+        wd.copy_(torch.from_numpy(w0))
+    o = run_oracle(shapes, "malt", W0, grads, hp)
+    for t, Gs in enumerate(grads):
+        Gd = [b[1:].view(s) for b, s in zip(bufG, shapes)]
+        for gd, gh in zip(Gd, Gs):
+            gd.copy_(torch.from_numpy(gh))
+        before = [x.double().cpu().numpy() for x in Wd]
+        plan.step(Wd, Gd, lm.make_hparams(**hp))
+        torch.cuda.synchronize()
+        for k in range(len(shapes)):
+            dW = Wd[k].double().cpu().numpy() - before[k]
+            assert rel_fro(dW, o[t]["inter"][k].dW) <= TOL_NS
+            assert rel_fro(plan.state_views(k)[0].double().cpu().numpy(), o[t]["M"][k]) <= TOL_STATE
+
+
+def test_c2_gpt2_small_full_set():
+    w = wl.WORKLOADS[2]
+    say(f"[parity] C2 gpt2-small {len(w.shapes)} matrices malt x1")
+    W0, grads = _inputs(w, 1)
+    g = run_gpu(list(w.shapes), w.variant, W0, grads, _hp(w))
+    o = run_oracle(list(w.shapes), w.variant, W0, grads, _hp(w))
+    worst = compare(g, o, w.variant, label="C2")
+    say(f"[parity] C2 worst {worst}")
+
+
+def test_c3_gpt2_medium_malter_sampled():
+    w = wl.WORKLOADS[3]
+    sample = [0, 1, 2, 3, 45, 50, 91, 95]
+    say(f"[parity] C3 gpt2-medium {len(w.shapes)} matrices malter x3, oracle on {sample}")
+    W0, grads = _inputs(w, 3)
+    g = run_gpu(list(w.shapes), w.variant, W0, grads, _hp(w), collect=sample)
+    o = run_oracle(list(w.shapes), w.variant, W0, grads, _hp(w), collect=sample)
+    worst = compare(g, o, w.variant, label="C3")
+    # MALTER's alpha departs from 1 after the first step.
+    assert abs(g[0].scal[0]["alpha"] - 1.0) < 1e-5
+    assert abs(g[2].scal[0]["alpha"] - 1.0) > 1e-3
+    say(f"[parity] C3 worst {worst}")
+
+
+def test_zero_gradients_leave_parameters_unchanged():
+    shapes = [(128, 300), (300, 128)]
+    say(f"[parity] zero grads {shapes}")
+    for variant in ("malt", "malter"):
+        W0 = [wl.weight(92, i, s) for i, s in enumerate(shapes)]
+        grads = [[np.zeros(s, np.float32) for s in shapes]]
+        g = run_gpu(shapes, variant, W0, grads, dict(lr=1e-2))
+        for k in range(len(shapes)):
+            assert np.all(np.isfinite(g[0].W[k]))
+            assert np.array_equal(g[0].W[k], W0[k].astype(np.float64))
+            assert g[0].scal[k]["graft"] == 0.0
+            assert np.all(g[0].Lv[k] == np.float32(10.0))
+
+
+def test_identity_preconditioner_matches_muon_reading():
+    shapes = [(256, 768), (384, 256)]
+    say(f"[parity] identity preconditioner {shapes}")
+    W0 = [wl.weight(93, i, s) for i, s in enumerate(shapes)]
+    grads = [[wl.grad(93, t, i, s) for i, s in enumerate(shapes)] for t in (1, 2)]
+    hp = dict(lr=2e-2, precond_identity=1)
+    g = run_gpu(shapes, "malt", W0, grads, hp)
+    o = run_oracle(shapes, "malt", W0, grads, hp)
+    compare(g, o, "malt", label="identity")
+    for st in g:
+        for k in range(len(shapes)):
+            assert np.all(st.Lv[k] == 1.0) and np.all(st.Rv[k] == 1.0)
+            assert abs(st.scal[k]["graft"] - 1.0) < 1e-6
+
+
+def test_single_ns_iteration_exposes_scaled_input():
+    # With one Newton-Schulz iteration X0 = bf16(L M R) is still in the workspace.
+    shapes = [(200, 520), (520, 200)]
+    say(f"[parity] ns_steps=1 {shapes}")
+    W0 = [wl.weight(94, i, s) for i, s in enumerate(shapes)]
+    grads = [[wl.grad(94, 1, i, s, "row_loguniform") for i, s in enumerate(shapes)]]
+    hp = dict(lr=1e-2, ns_steps=1)
+    g = run_gpu(shapes, "malt", W0, grads, hp)
+    o = run_oracle(shapes, "malt", W0, grads, hp)
+    compare(g, o, "malt", tol_ns=8e-3, label="ns1")
+    for k in range(len(shapes)):
+        # bf16 rounding only: relative error <= 2^-9 per entry.
+        assert rel_fro(g[0].X0[k], o[0]["inter"][k].M_tilde) < 2.0 ** -9
+
+
+def test_weight_decay_reading():
+    shapes = [(256, 512)]
+    say("[parity] weight decay")
+    W0 = [wl.weight(95, 0, shapes[0])]
+    grads = [[wl.grad(95, t, 0, shapes[0])] for t in (1, 2)]
+    hp = dict(lr=1e-2, weight_decay=0.1)
+    g = run_gpu(shapes, "malt", W0, grads, hp)
+    o = run_oracle(shapes, "malt", W0, grads, hp)
+    compare(g, o, "malt", label="wd")
+
+
+def test_graft_identity_on_gpu_scalars():
+    # ||dW|| = lr * alpha * ||O|| ||D|| / (||D|| + eps), with the GPU's own O.
+    w = wl.WORKLOADS[2]
+    idx = [0, 1, 2, 3]
+    shapes = [w.shapes[i] for i in idx]
+    say(f"[parity] graft identity {shapes}")
+    W0 = [wl.weight(2, i, s) for i, s in zip(idx, shapes)]
+    grads = [[wl.grad(2, 1, i, s) for i, s in zip(idx, shapes)]]
+    g = run_gpu(shapes, "malter", W0, grads, dict(lr=w.lr))
+    for k in range(len(shapes)):
+        O = g[0].O[k]
+        D = g[0].Lv[k][:, None] * O * g[0].Rv[k][None, :]
+        nO, nD = np.linalg.norm(O), np.linalg.norm(D)
+        assert abs(np.sqrt(g[0].scal[k]["o2"]) - nO) / nO < 1e-5
+        assert abs(np.sqrt(g[0].scal[k]["d2"]) - nD) / nD < 1e-5
+        expect = w.lr * g[0].scal[k]["alpha"] * nO * nD / (nD + 1e-8)
+        assert abs(np.linalg.norm(g[0].dW[k]) - expect) / expect < 1e-3

@@ -1,0 +1,127 @@
+"""Runtime properties of libmalt on the GPU: determinism, checkpoint/resume,
+independence of matrices, error paths and per-phase timing."""
+import numpy as np
+import pytest
+
+from gpu_harness import run_gpu, say, to_dev
+from paper_2608_05088_amd import libmalt as lm
+from paper_2608_05088_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    lm.lib()
+
+
+SHAPES = [(768, 2304), (768, 768), (300, 1000), (1000, 300), (7, 33)]
+
+
+def _inputs(steps, cid=96):
+    W0 = [wl.weight(cid, i, s) for i, s in enumerate(SHAPES)]
+    grads = [[wl.grad(cid, t, i, s, "student_t3") for i, s in enumerate(SHAPES)] for t in range(1, steps + 1)]
+    return W0, grads
+
+
+def test_bitwise_deterministic():
+    say("[runtime] determinism")
+    W0, grads = _inputs(2)
+    a = run_gpu(SHAPES, "malter", W0, grads, dict(lr=6e-3))
+    b = run_gpu(SHAPES, "malter", W0, grads, dict(lr=6e-3))
+    for sa, sb in zip(a, b):
+        for k in range(len(SHAPES)):
+            assert np.array_equal(sa.W[k], sb.W[k])
+            assert np.array_equal(sa.M[k], sb.M[k])
+            assert np.array_equal(sa.l[k], sb.l[k]) and np.array_equal(sa.r[k], sb.r[k])
+            assert sa.nu[k] == sb.nu[k]
+
+
+def test_checkpoint_resume_is_bitwise():
+    import torch
+    say("[runtime] checkpoint/resume")
+    W0, grads = _inputs(3)
+    hp = lm.make_hparams(lr=6e-3)
+    ref = run_gpu(SHAPES, "malter", W0, grads, dict(lr=6e-3))
+    plan = lm.Plan(SHAPES, "malter")
+    Wd = to_dev(W0)
+    for Gs in grads[:2]:
+        plan.step(Wd, to_dev(Gs), hp)
+    torch.cuda.synchronize()
+    saved_state = plan.state.clone()
+    saved_W = [w.clone() for w in Wd]
+    t = plan.t
+    plan.close()
+    plan2 = lm.Plan(SHAPES, "malter", state=saved_state, from_existing=True, step=t)
+    assert plan2.t == 2
+    plan2.step(saved_W, to_dev(grads[2]), hp)
+    torch.cuda.synchronize()
+    for k in range(len(SHAPES)):
+        assert np.array_equal(saved_W[k].double().cpu().numpy(), ref[2].W[k])
+
+
+def test_matrices_are_independent():
+    say("[runtime] subset independence")
+    W0, grads = _inputs(2)
+    full = run_gpu(SHAPES, "malt", W0, grads, dict(lr=1e-2))
+    sub_idx = [1, 3]
+    sub = run_gpu([SHAPES[i] for i in sub_idx], "malt", [W0[i] for i in sub_idx],
+                  [[g[i] for i in sub_idx] for g in grads], dict(lr=1e-2))
+    for t in range(2):
+        for k, i in enumerate(sub_idx):
+            assert np.array_equal(sub[t].W[k], full[t].W[i])
+
+
+def test_errors_leave_state_untouched():
+    import torch
+    say("[runtime] error paths")
+    shapes = [(64, 96), (96, 64)]
+    plan = lm.Plan(shapes, "malt")
+    W = to_dev([wl.weight(97, i, s) for i, s in enumerate(shapes)])
+    G = to_dev([wl.grad(97, 1, i, s) for i, s in enumerate(shapes)])
+    before = plan.state.clone()
+    with pytest.raises(lm.MaltError) as e:
+        plan._c_shapes[0].rows = 65
+        plan.step(W, G)
+    assert e.value.status == lm.MALT_ERR_STATE_MISMATCH
+    plan._c_shapes[0].rows = 64
+    with pytest.raises(lm.MaltError) as e:
+        plan.step([W[0], W[0]], G)            # in-place outputs overlap
+    assert e.value.status in (lm.MALT_ERR_ALIAS, lm.MALT_ERR_STATE_MISMATCH)
+    with pytest.raises(lm.MaltError) as e:
+        plan.step(W, G, lm.make_hparams(mu1=1.0))
+    assert e.value.status == lm.MALT_ERR_INVALID_ARG
+    with pytest.raises(lm.MaltError) as e:
+        plan.step(W, G, lm.make_hparams(ns_steps=0))
+    assert e.value.status == lm.MALT_ERR_INVALID_ARG
+    with pytest.raises(lm.MaltError) as e:
+        plan.step([W[0], G[1]], G)            # a param aliases a grad
+    assert e.value.status == lm.MALT_ERR_ALIAS
+    torch.cuda.synchronize()
+    assert plan.t == 0
+    assert torch.equal(plan.state, before)
+    plan.step(W, G)
+    torch.cuda.synchronize()
+    assert plan.t == 1
+
+
+def test_profile_counts_every_launch():
+    import torch
+    say("[runtime] profiling")
+    shapes = [(256, 512), (512, 256)]
+    plan = lm.Plan(shapes, "malt")
+    W = to_dev([wl.weight(98, i, s) for i, s in enumerate(shapes)])
+    plan.profile_enable(True)
+    for t in (1, 2):
+        plan.step(W, to_dev([wl.grad(98, t, i, s) for i, s in enumerate(shapes)]))
+    torch.cuda.synchronize()
+    prof = plan.profile_read()
+    assert prof["ns_gram"]["launches"] == 10 and prof["ns_update"]["launches"] == 10
+    assert prof["momentum_rowcol"]["launches"] == 2 and prof["backmap_write"]["launches"] == 2
+    assert all(v["ms"] >= 0 for v in prof.values())
+    assert prof["ns_update"]["flops"] == 5 * 2.0 * 2 * 256 * 256 * 512
+    again = plan.profile_read()
+    assert again["ns_gram"]["launches"] == 0
