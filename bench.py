@@ -36,7 +36,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="gpt2_large")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-layers", type=int, default=1)
+    ap.add_argument("--cpu-sample-layers", type=int, default=12)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after timing, run one plain 1 GiB device-to-device copy (HBM counter calibration)")
     return ap.parse_args()
 
 
@@ -172,6 +174,13 @@ def main():
     plan.close()
     del grad_sets, Wd
     torch.cuda.empty_cache()
+    if args.copy_calibration:
+        # A plain copy of known size: 2^30 bytes read, 2^30 bytes written.
+        src = torch.ones(2 ** 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -135,14 +135,18 @@ malt_status_t malt_state_layout(const malt_plan_t* plan, int32_t i, malt_state_l
 /* Byte offsets into workspace_mem of matrix i's last-step intermediates,
  * for stage-by-stage checks:
  *  Lv, Rv:  float32 diagonals of L_t (rows) and R_t (cols);
- *  O:       bf16 Newton-Schulz output in W's orientation, rows x cols with a
- *           row pitch of O_pitch elements;
- *  X0:      bf16 L M R before normalisation, same orientation and pitch;
+ *  O:       bf16 Newton-Schulz output in the canonical orientation:
+ *           min(rows,cols) x max(rows,cols), row pitch O_pitch elements; it is
+ *           W's orientation when rows <= cols and its transpose otherwise
+ *           (O_transposed = 1);
+ *  X0:      bf16 L M R before normalisation, same layout; valid only after a
+ *           step with ns_steps == 1 (later iterations reuse the buffer);
  *  scalars: float64 [s=||Mt||_F, sigma=1/(s+ns_eps), nu_t, alpha_t, ||O||^2,
  *           ||D||^2, graft=||O||/(||D||+eps), coef=lr*alpha*graft]. */
 typedef struct {
   int64_t Lv, Rv, O, X0, scalars;
   int64_t O_pitch;
+  int64_t O_transposed;
 } malt_debug_layout_t;
 malt_status_t malt_debug_layout(const malt_plan_t* plan, int32_t i, malt_debug_layout_t* out);
 

@@ -1,8 +1,8 @@
 // HBM-bound passes of the MALT / MALTER step (gfx950):
 //   momentum_rowcol   M <- mu1 M + (1-mu1) G, per-tile row and column sums of G^2
 //   precond_finalize  l, r EMAs and L = (l+eps)^(-1/8), R = (r+eps)^(-1/8)
-//   scale_convert     X0 = bf16(L M R) in both orientations, ||LMR||^2 and
-//                     (MALTER) ||LGR||^2 partials
+//   scale_convert     X0 = bf16(L M R) in the canonical orientation, ||LMR||^2
+//                     and (MALTER) ||LGR||^2 partials
 //   norm_scalars      s, sigma, nu_t, alpha_t per matrix
 //   graft_scalars     ||O||, ||D||, graft and step coefficient per matrix
 //   backmap_write     W <- decay W - coef * L O R
@@ -126,9 +126,10 @@ __global__ __launch_bounds__(NTHREADS) void precond_finalize_kernel(EwArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// X0 = bf16(L M R) written in W's orientation and transposed (through LDS),
-// over the zero-padded domain; per-tile sums of (LMR)^2 and, for MALTER,
-// (LGR)^2.  Tiles cover W-oriented padded rows x cols in K2_T x K2_T blocks.
+// X0 = bf16(L M R) in the canonical orientation (W for wide matrices, W^T
+// through an LDS transpose for tall ones) over the zero-padded domain, plus
+// per-tile sums of (LMR)^2 and, for MALTER, (LGR)^2.  Tiles cover W-oriented
+// padded rows x cols in K2_T x K2_T blocks.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(NTHREADS) void scale_convert_kernel(EwArgs a) {
   __shared__ bf16_t tsh[K2_T][K2_T + 2];
@@ -137,10 +138,8 @@ __global__ __launch_bounds__(NTHREADS) void scale_convert_kernel(EwArgs a) {
   const MatDesc& d = a.desc[t.mat];
   const int m = d.m, n = d.n;
   const bool vec = a.ptrs[t.mat].vec != 0;
-  bf16_t* __restrict__ Wo = d.tall ? d.XT[0] : d.X[0];
-  bf16_t* __restrict__ Tr = d.tall ? d.X[0] : d.XT[0];
-  const int pw = d.tall ? d.mp : d.np;   // row pitch of the W-oriented buffer (padded cols)
-  const int pt = d.tall ? d.np : d.mp;   // row pitch of the transposed buffer (padded rows)
+  bf16_t* __restrict__ X0 = d.X[0];
+  const int ldx = d.np;                  // canonical row pitch
   const float* __restrict__ G = a.ptrs[t.mat].G;
   const int r0 = t.ti * K2_T, c0 = t.tj * K2_T;
   const int cc = (threadIdx.x & 15) * 4;
@@ -174,25 +173,27 @@ __global__ __launch_bounds__(NTHREADS) void scale_convert_kernel(EwArgs a) {
     }
     bf16_t h[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      h[e] = f2bf(x[e]);
-      tsh[rr][cc + e] = h[e];
+    for (int e = 0; e < 4; ++e) h[e] = f2bf(x[e]);
+    if (!d.tall) {
+      uint2 pk;
+      pk.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
+      pk.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
+      *reinterpret_cast<uint2*>(X0 + (size_t)r * ldx + c0 + cc) = pk;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) tsh[rr][cc + e] = h[e];
     }
-    uint2 pk;
-    pk.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
-    pk.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
-    *reinterpret_cast<uint2*>(Wo + (size_t)r * pw + c0 + cc) = pk;
   }
-  __syncthreads();
-  // Transposed write: thread -> (column ct, 16-row segment).
-  {
+  if (d.tall) {
+    __syncthreads();
+    // Transposed write: thread -> (W column ct, 16-row segment).
     const int ct = threadIdx.x >> 2;
     const int seg = (threadIdx.x & 3) * 16;
     uint32_t wv[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k)
       wv[k] = (uint32_t)tsh[seg + 2 * k][ct] | ((uint32_t)tsh[seg + 2 * k + 1][ct] << 16);
-    uint4* dst = reinterpret_cast<uint4*>(Tr + (size_t)(c0 + ct) * pt + r0 + seg);
+    uint4* dst = reinterpret_cast<uint4*>(X0 + (size_t)(c0 + ct) * ldx + r0 + seg);
     dst[0] = make_uint4(wv[0], wv[1], wv[2], wv[3]);
     dst[1] = make_uint4(wv[4], wv[5], wv[6], wv[7]);
   }
@@ -269,20 +270,39 @@ __global__ __launch_bounds__(NTHREADS) void graft_scalars_kernel(EwArgs a) {
 
 // ---------------------------------------------------------------------------
 // W <- decay * W - coef * L_i O_ij R_j  (Alg. 1/2, last line; D = L O R).
-// Reads W and O (bf16), writes W: 10 bytes per element.
+// O is the bf16 canonical Newton-Schulz output: W-oriented for wide matrices,
+// W^T for tall ones (read through an LDS transpose).  Reads W and O, writes
+// W: 10 bytes per element.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(NTHREADS) void backmap_write_kernel(EwArgs a) {
+  __shared__ bf16_t osh[EW_TC][EW_TR + 2];   // tall: O^T block, [W col][W row]
   const Tile t = a.tiles[xcd_remap(blockIdx.x, gridDim.x)];
   const MatDesc& d = a.desc[t.mat];
   const int m = d.m, n = d.n;
   const bool vec = a.ptrs[t.mat].vec != 0;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int r0 = t.ti * EW_TR, c = t.tj * EW_TC + lane * 4;
-  const bf16_t* __restrict__ O = d.tall ? d.XT[a.o_parity] : d.X[a.o_parity];
-  const int po = d.tall ? d.mp : d.np;
+  const int r0 = t.ti * EW_TR, c0 = t.tj * EW_TC, c = c0 + lane * 4;
+  const bf16_t* __restrict__ O = d.X[a.o_parity];
+  const int ldo = d.np;
   float* __restrict__ W = a.ptrs[t.mat].W;
   const float coef = (float)d.scal[SC_COEF];
   const float decay = a.decay;
+  if (d.tall) {
+    // Canonical rows c0 .. c0+255 (W columns), columns r0 .. r0+31 (W rows):
+    // one 64-byte row segment per thread (inside the padded buffer).
+    const uint4* srow = reinterpret_cast<const uint4*>(O + (size_t)(c0 + threadIdx.x) * ldo + r0);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint4 v = srow[q];
+      const uint32_t vw[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        osh[threadIdx.x][q * 8 + 2 * k] = (bf16_t)(vw[k] & 0xffffu);
+        osh[threadIdx.x][q * 8 + 2 * k + 1] = (bf16_t)(vw[k] >> 16);
+      }
+    }
+    __syncthreads();
+  }
   float Rv[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) Rv[e] = (c + e < n) ? d.Rv[c + e] : 0.f;
@@ -292,9 +312,17 @@ __global__ __launch_bounds__(NTHREADS) void backmap_write_kernel(EwArgs a) {
     const float cl = coef * d.Lv[r];
     float wv[4];
     load4(W + (size_t)r * n, c, n, vec, wv);
-    const uint2 pk = *reinterpret_cast<const uint2*>(O + (size_t)r * po + c);
-    const float o[4] = {bf2f((bf16_t)(pk.x & 0xffffu)), bf2f((bf16_t)(pk.x >> 16)),
-                        bf2f((bf16_t)(pk.y & 0xffffu)), bf2f((bf16_t)(pk.y >> 16))};
+    float o[4];
+    if (!d.tall) {
+      const uint2 pk = *reinterpret_cast<const uint2*>(O + (size_t)r * ldo + c);
+      o[0] = bf2f((bf16_t)(pk.x & 0xffffu));
+      o[1] = bf2f((bf16_t)(pk.x >> 16));
+      o[2] = bf2f((bf16_t)(pk.y & 0xffffu));
+      o[3] = bf2f((bf16_t)(pk.y >> 16));
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = bf2f(osh[lane * 4 + e][rr]);
+    }
 #pragma unroll
     for (int e = 0; e < 4; ++e) wv[e] = decay * wv[e] - cl * o[e] * Rv[e];
     store4(W + (size_t)r * n, c, n, vec, wv);

@@ -50,7 +50,7 @@ struct MatPlan {
   // offsets
   int64_t st_M, st_l, st_r, st_nu;     // floats from state base
   size_t ws_scal, ws_Lv, ws_Rv, ws_rowpart, ws_colpart, ws_k2part, ws_gpart;
-  size_t ws_X[2], ws_XT[2], ws_A, ws_B;
+  size_t ws_X[2], ws_A, ws_B;
   // algorithmic cost
   double ns_flops_sym_per_iter;        // 3 mc^2 nc + mc^3 (symmetric minimum)
 };
@@ -130,7 +130,6 @@ Layout make_layout(const malt_shape_t* shapes, int32_t n, malt_variant_t variant
     p.ws_k2part = take(8 * size_t(p.k2_tiles));
     p.ws_gpart = take(8 * size_t(p.upd_tiles));
     for (int b = 0; b < 2; ++b) p.ws_X[b] = take(2 * size_t(p.mp) * p.np);
-    for (int b = 0; b < 2; ++b) p.ws_XT[b] = take(2 * size_t(p.mp) * p.np);
     p.ws_A = take(2 * size_t(p.mp) * p.mp);
     p.ws_B = take(2 * size_t(p.mp) * p.mp * (p.split ? 2 : 1));
   }
@@ -247,10 +246,7 @@ void fill_desc(const malt_plan* p, std::vector<MatDesc>& D) {
     d.colpart = reinterpret_cast<float*>(w + q.ws_colpart);
     d.k2part = reinterpret_cast<float*>(w + q.ws_k2part);
     d.gpart = reinterpret_cast<float*>(w + q.ws_gpart);
-    for (int b = 0; b < 2; ++b) {
-      d.X[b] = reinterpret_cast<bf16_t*>(w + q.ws_X[b]);
-      d.XT[b] = reinterpret_cast<bf16_t*>(w + q.ws_XT[b]);
-    }
+    for (int b = 0; b < 2; ++b) d.X[b] = reinterpret_cast<bf16_t*>(w + q.ws_X[b]);
     d.A = reinterpret_cast<bf16_t*>(w + q.ws_A);
     d.B = reinterpret_cast<bf16_t*>(w + q.ws_B);
     d.scal = reinterpret_cast<double*>(w + q.ws_scal);
@@ -534,9 +530,10 @@ malt_status_t malt_debug_layout(const malt_plan_t* p, int32_t i, malt_debug_layo
   const int par = p->last_ns_steps & 1;
   out->Lv = int64_t(q.ws_Lv);
   out->Rv = int64_t(q.ws_Rv);
-  out->O = int64_t(q.tall ? q.ws_XT[par] : q.ws_X[par]);
-  out->X0 = int64_t(q.tall ? q.ws_XT[0] : q.ws_X[0]);
-  out->O_pitch = q.tall ? q.mp : q.np;
+  out->O = int64_t(q.ws_X[par]);
+  out->X0 = int64_t(q.ws_X[0]);
+  out->O_pitch = q.np;
+  out->O_transposed = q.tall ? 1 : 0;
   out->scalars = int64_t(q.ws_scal);
   return MALT_OK;
 }
@@ -564,7 +561,7 @@ malt_status_t malt_profile_read(malt_plan_t* p, malt_profile_t* out, int32_t res
     const double el = double(q.m) * q.n, mn = double(q.m + q.n);
     out->bytes[0] += 12.0 * el + 4.0 * mn;                      // G, M in; M out; row/col partials
     out->bytes[1] += 8.0 * mn + 4.0 * mn;                       // l, r in/out, L, R out
-    out->bytes[2] += (malter ? 8.0 : 4.0) * el + 4.0 * el;      // M (+G) in; X0 in two orientations
+    out->bytes[2] += (malter ? 8.0 : 4.0) * el + 2.0 * el;      // M (+G) in; bf16 X0 out
     out->bytes[8] += 10.0 * el;                                 // W, O in; W out
     const int steps = p->last_ns_steps;
     out->flops[4] += steps * double(q.mc) * q.mc * q.nc;            // X X^T, one triangle

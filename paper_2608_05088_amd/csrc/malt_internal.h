@@ -58,8 +58,7 @@ struct MatDesc {
   float* colpart;      // [k1_rt][n]
   float* k2part;       // [k2_tiles][2]: sum (LMR)^2, sum (LGR)^2
   float* gpart;        // [upd_tiles][2]: sum O^2, sum (LOR)^2
-  bf16_t* X[2];        // canonical mp x np, row-major
-  bf16_t* XT[2];       // canonical transpose np x mp, row-major
+  bf16_t* X[2];        // canonical mp x np, row-major (double-buffered iterate)
   bf16_t* A;           // mp x mp  (Gram / A)
   bf16_t* B;           // mp x mp, or mp x 2mp [hi | lo] when split (b A + c A^2)
   double* scal;        // MAT_SCALARS
@@ -97,7 +96,7 @@ struct EwArgs {
   float decay;           // 1 - lr * weight_decay
   int32_t malter;
   int32_t identity;
-  int32_t o_parity;      // which X/XT buffer holds the final O
+  int32_t o_parity;      // which X buffer holds the final O
 };
 
 struct NsArgs {
@@ -107,7 +106,7 @@ struct NsArgs {
   int32_t phase;
   int32_t first;         // iteration 0: apply sigma
   int32_t last;          // final iteration: write O and graft partials
-  int32_t src;           // X[src] / XT[src] is the current iterate
+  int32_t src;           // X[src] is the current iterate, X[src ^ 1] receives the next
   float a, b, c;
 };
 

@@ -1,41 +1,75 @@
 // Grouped Newton-Schulz GEMMs on the gfx950 matrix cores (bf16 in, fp32 acc).
 //
-// Every phase is one launch over all matrices of the step; every workgroup
-// computes one 256 x 256 output tile C = P Q^T with P, Q row-major bf16 and
-// the contraction index contiguous in both (an "NT" product):
-//   Gram:       A = s X X^T            (P = Q = X, symmetric: upper tiles only,
-//                                        mirrored on write; s = sigma^2 on the
-//                                        first iteration, else 1)
-//   Polynomial: B = b A + c A A^T      (A symmetric, so A A = A A^T; upper tiles)
-//   Update:     X' = s (a X + B X)     (Q = X^T, the stored transpose; s = sigma
-//                                        on the first iteration)
-// X is kept in both orientations so that every product reads its operands
-// along contiguous rows; the update writes both orientations of X', and on
-// the last iteration only the one in W's orientation plus the per-tile sums
-// of O^2 and (L O R)^2 used by norm grafting.
+// One Newton-Schulz iteration (Muon's quintic) on the canonical X (mp x np,
+// rows <= cols, zero-padded to multiples of 256) is three grouped launches,
+// each over every matrix of the step, one 256 x 256 output tile per
+// workgroup:
+//   Gram        A  = s X X^T                 NT product, symmetric: upper tiles
+//                                            only, mirrored on write; s = sigma^2
+//                                            on the first iteration, else 1
+//   Polynomial  B' = a I + b A + c A A^T     NT product (A is symmetric, so
+//                                            A A = A A^T); upper tiles, mirrored
+//   Update      X' = s B' X                  NN product; s = sigma on the first
+//                                            iteration
+// Folding a X into B' = a I + B makes X' a single product: X' needs no
+// addend, and every iteration applies one rounded matrix to one rounded X.
+// A, B' and X are bf16 (round to nearest even).
 //
-// Rounding: A, B and X are stored as bf16 (round to nearest even) and the
-// same rounded A feeds both terms of B, the same rounded X both terms of X'.
+// Main loop (all three): 8 waves (2 per SIMD), each owning a 128 x 64 sub-tile
+// as 32x32 blocks of v_mfma_f32_32x32x16_bf16.  Operand stages of BK k-values
+// stream from global memory straight into an LDS ring (global_load_lds,
+// 16 bytes per lane), STAGES deep, one barrier per stage; fragments are
+// double-buffered in registers so the reads for the next 16-k sub-step are in
+// flight while the current one multiplies.
 //
-// Workgroup: 256 threads = 4 waves in a 2 x 2 arrangement, each wave owning a
-// 128 x 128 sub-tile as 4 x 4 blocks of v_mfma_f32_32x32x16_bf16.  K advances
-// in steps of 64 through two LDS stages (rows padded to 72 bf16 so that the
-// 16-byte fragment reads of 16 consecutive rows hit distinct banks); global
-// loads for step k+1 are in flight while step k is multiplied.
+// NT operands (rows with k contiguous) use ds_read_b128 fragments from an
+// XOR-swizzled [row][k] tile.  The update reads X as a row-major [k][n]
+// stage tile and builds the MFMA A operand with ds_read_b64_tr_b16 transposed
+// reads; it computes C^T = X^T B' so every lane holds four consecutive output
+// columns of one row and stores them straight from registers.
+#include <type_traits>
+
 #include "malt_internal.h"
 
 namespace malt {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 
-constexpr int LDS_STRIDE = NS_BK + 8;                 // bf16 per LDS row
-constexpr int STAGE_ELEMS = NS_TILE * LDS_STRIDE;    // one operand, one stage
-constexpr int LDS_BYTES = 2 * 2 * STAGE_ELEMS * 2;   // 2 stages x (P, Q) x bf16
+#ifndef MALT_NS_BK
+#define MALT_NS_BK 64
+#endif
+#ifndef MALT_NS_STAGES
+#define MALT_NS_STAGES 2
+#endif
+constexpr int NW = 8;                                // waves per workgroup
+constexpr int NT = NW * 64;                          // threads per workgroup
+constexpr int BK = MALT_NS_BK;                       // k per pipeline stage
+constexpr int STAGES = MALT_NS_STAGES;               // LDS ring depth
+constexpr int H = BK / 16;                           // MFMA sub-steps per stage
+constexpr int RB = BK * 2;                           // bytes per [row][k] tile row
+constexpr int CPR = BK / 8;                          // 16-byte chunks per [row][k] row
+constexpr int RPP = 256 / RB;                        // [row][k] rows per 256-byte bank period
+constexpr int KN_ROW = NS_TILE * 2;                  // bytes per [k][n] tile row (512)
+constexpr int OPER_BYTES = NS_TILE * BK * 2;         // one operand tile of one stage
+constexpr int STAGE_BYTES = 2 * OPER_BYTES;
+constexpr int RING_BYTES = STAGES * STAGE_BYTES;
+constexpr int LOADS = 2 * OPER_BYTES / 1024 / NW;    // 1 KB direct loads per wave per stage
 constexpr int EPI_F = NS_TILE + 4;                   // fp32 epilogue stage row (floats)
 constexpr int EPI_B = NS_TILE + 8;                   // bf16 epilogue stage row
-static_assert(64 * EPI_F * 4 + 2 * 64 * EPI_B * 2 <= LDS_BYTES, "epilogue stage exceeds LDS");
+constexpr int EPI_BYTES = 64 * EPI_F * 4 + 2 * 64 * EPI_B * 2;
+constexpr int LDS_BYTES = RING_BYTES > EPI_BYTES ? RING_BYTES : EPI_BYTES;
+static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
+static_assert(H % 2 == 0, "sub-steps per stage must be even");
+static_assert(LOADS * NW * 1024 == 2 * OPER_BYTES, "loads must split evenly over the waves");
+
+// Wave grid 2 x 4: each wave owns TM x TN of the 256 x 256 tile.
+constexpr int TM = NS_TILE / 2, TN = NS_TILE / 4;
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4_t;
+typedef __attribute__((address_space(1))) void gbl_void_t;
 
 __device__ __forceinline__ bf16_t f2bf_rne(float x) {
   uint32_t u = __float_as_uint(x);
@@ -51,165 +85,214 @@ __device__ __forceinline__ float wsum(float v) {
   return v;
 }
 
-__global__ __launch_bounds__(NTHREADS, 1) void ns_gemm_kernel(NsArgs args) {
-  extern __shared__ __attribute__((aligned(16))) bf16_t lds[];
+// Wait until at most n (<= 63) of this wave's vector-memory loads are in flight.
+#define MALT_VM_CASE(k) case k: asm volatile("s_waitcnt vmcnt(" #k ")" ::: "memory"); break;
+__device__ __forceinline__ void wait_vm(int n) {
+  switch (n) {
+    MALT_VM_CASE(0) MALT_VM_CASE(1) MALT_VM_CASE(2) MALT_VM_CASE(3) MALT_VM_CASE(4) MALT_VM_CASE(5)
+    MALT_VM_CASE(6) MALT_VM_CASE(7) MALT_VM_CASE(8) MALT_VM_CASE(9) MALT_VM_CASE(10) MALT_VM_CASE(11)
+    MALT_VM_CASE(12) MALT_VM_CASE(13) MALT_VM_CASE(14) MALT_VM_CASE(15) MALT_VM_CASE(16)
+    MALT_VM_CASE(18) MALT_VM_CASE(20) MALT_VM_CASE(24) MALT_VM_CASE(28) MALT_VM_CASE(32)
+    MALT_VM_CASE(36) MALT_VM_CASE(40) MALT_VM_CASE(48) MALT_VM_CASE(56)
+    default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+  }
+}
+#undef MALT_VM_CASE
+
+// Compile-time vmcnt wait (gfx9 s_waitcnt encoding: vmcnt[3:0] and [15:14],
+// expcnt and lgkmcnt left at their maxima, i.e. not waited on).
+template <int N>
+__device__ __forceinline__ void wait_vm_c() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// [row][k] tile (NT operands): 256 rows x BK bf16, CPR 16-byte chunks per row,
+// chunk kc stored at kc ^ ((row / RPP) % CPR): the ds_read_b128 fragment reads
+// of 16 consecutive rows at one chunk hit 16 distinct 4-bank groups.
+__device__ __forceinline__ int swz_rk(int row, int kc) { return row * RB + ((kc ^ ((row / RPP) % CPR)) << 4); }
+
+// [k][n] tile (X in the update): BK rows of 256 bf16 (512 bytes), 16-byte chunk
+// c stored at c ^ (4 * (k & 3)): the 16 lanes of one transposed read (four
+// rows x 32 contiguous bytes) hit 16 distinct 4-bank groups.
+__device__ __forceinline__ int swz_kn(int k, int n) {
+  return k * KN_ROW + (((n >> 3) ^ (4 * (k & 3))) << 4) + ((n & 7) << 1);
+}
+
+// Software pipeline over KT stages shared by both kernels.
+//   issue(kt)        start the direct loads of stage kt into slot kt % STAGES
+//   read(buf, st, h) fragment reads of sub-step h of the stage at st into buf
+//   mma(buf)         the MFMAs of the fragments in buf
+// At the barrier inside iteration kt, stages up to kt + STAGES - 1 have been
+// issued and stage kt + 1 is awaited; after it, slot kt % STAGES (already
+// read by every wave) receives stage kt + STAGES.
+template <class Issue, class Read, class Mma>
+__device__ __forceinline__ void pipeline(const int KT, char* lds, Issue&& issue, Read&& read, Mma&& mma) {
+  auto ahead = [&](int j) { return min(STAGES - 2, KT - 1 - j); };
+#pragma unroll
+  for (int s = 0; s < STAGES; ++s)
+    if (s < KT) issue(s);
+  wait_vm(min(STAGES - 1, KT - 1) * LOADS);
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  read(0, lds, 0);
+  auto body = [&](const int kt, auto steady_tag) {
+    constexpr bool steady = decltype(steady_tag)::value;
+    const char* st = lds + (kt % STAGES) * STAGE_BYTES;
+#pragma unroll
+    for (int h = 0; h < H; ++h) {
+      const int c = h & 1;
+      if (h + 1 < H) {
+        read(c ^ 1, st, h + 1);
+      } else if (steady || kt + 1 < KT) {
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // this wave's reads of stage kt are done
+        if constexpr (steady) wait_vm_c<(STAGES - 2) * LOADS>();
+        else wait_vm(ahead(kt + 1) * LOADS);
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        if constexpr (steady) issue(kt + STAGES);
+        read(c ^ 1, lds + ((kt + 1) % STAGES) * STAGE_BYTES, 0);
+      }
+      mma(c);
+    }
+  };
+  int kt = 0;
+  for (; kt < KT - STAGES; ++kt) body(kt, std::true_type{});
+  for (; kt < KT; ++kt) body(kt, std::false_type{});
+}
+
+// ===========================================================================
+// Gram and polynomial phases: C = P Q^T, symmetric output, upper tiles.
+// ===========================================================================
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void ns_gemm_sym_kernel(NsArgs args) {
+  constexpr int I = TM / 32, J = TN / 32;    // 32x32 blocks per wave
+  constexpr int ROWS_PER_LOAD = 1024 / RB;
+  constexpr int LOADS_PER_OPER = NS_TILE / ROWS_PER_LOAD;
+
+  extern __shared__ __attribute__((aligned(16))) char lds[];
   const Tile t = args.tiles[xcd_remap(blockIdx.x, gridDim.x)];
   const MatDesc& d = args.desc[t.mat];
   const int phase = args.phase;
   const int mp = d.mp, np = d.np;
-
-  const bf16_t* P;
-  const bf16_t* Q;
-  int ldp, ldq, K;
-  if (phase == PH_GRAM) {
-    P = d.X[args.src]; Q = P; ldp = ldq = np; K = np;
-  } else if (phase == PH_POLY) {
-    P = d.A; Q = P; ldp = ldq = mp; K = mp;
-  } else {
-    // Split matrices contract over [B_hi | B_lo] and [X^T | X^T]: K = 2 mp.
-    P = d.B; Q = d.XT[args.src]; ldq = mp;
-    ldp = d.split ? 2 * mp : mp;
-    K = d.split ? 2 * mp : mp;
-  }
-  const int kwrap = (phase == PH_UPDATE) ? mp : K;   // Q's k index wraps at mp
+  const bf16_t* P = (phase == PH_GRAM) ? d.X[args.src] : d.A;
+  const int ld = (phase == PH_GRAM) ? np : mp;
+  const int K = ld;
   const int row0 = t.ti * NS_TILE, col0 = t.tj * NS_TILE;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wr = wave >> 1, wc = wave & 1;
+  const int wr = wave / 4, wc = wave % 4;
 
-  // Global -> LDS mapping: 8 threads per 64-wide row (16 B each), 32 rows per pass.
-  const int lrow = tid >> 3, lchunk = (tid & 7) * 8;
-  const bf16_t* gp = P + (size_t)(row0 + lrow) * ldp + lchunk;
-  const bf16_t* gq = Q + (size_t)(col0 + lrow) * ldq + lchunk;
-  u32x4 rp[8], rq[8];
-
-  // Stage b holds P at lds + 2b*STAGE_ELEMS and Q right after it.
-
-  f32x16 acc[4][4];
+  // Direct-load sources: instruction g < LOADS_PER_OPER covers rows of the
+  // tile-row panel, the rest rows of the tile-column panel (both of P).
+  const bf16_t* src[LOADS];
+  int dst_off[LOADS];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int q = 0; q < LOADS; ++q) {
+    const int g = wave + q * NW;
+    const int op = g / LOADS_PER_OPER, qi = g % LOADS_PER_OPER;
+    const int row = qi * ROWS_PER_LOAD + lane / CPR;
+    const int kc = (lane % CPR) ^ ((row / RPP) % CPR);
+    src[q] = P + (size_t)((op ? col0 : row0) + row) * ld + kc * 8;
+    dst_off[q] = op * OPER_BYTES + qi * 1024;
+  }
+  int offa[I][H], offb[J][H];
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+  for (int h = 0; h < H; ++h) {
+    const int kc = 2 * h + (lane >> 5);
+#pragma unroll
+    for (int i = 0; i < I; ++i) offa[i][h] = swz_rk(wr * TM + i * 32 + (lane & 31), kc);
+#pragma unroll
+    for (int j = 0; j < J; ++j) offb[j][h] = OPER_BYTES + swz_rk(wc * TN + j * 32 + (lane & 31), kc);
+  }
+
+  f32x16 acc[I][J];
+#pragma unroll
+  for (int i = 0; i < I; ++i)
+#pragma unroll
+    for (int j = 0; j < J; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+  bf16x8 fa[2][I], fb[2][J];
 
-  const int frow = lane & 31, fk = (lane >> 5) * 8;
-  const int KT = K / NS_BK;
-#define NS_GLOAD(k0)                                                                  \
-  _Pragma("unroll") for (int p = 0; p < 8; ++p) {                                      \
-    rp[p] = *reinterpret_cast<const u32x4*>(gp + (size_t)(32 * p) * ldp + (k0));       \
-    rq[p] = *reinterpret_cast<const u32x4*>(gq + (size_t)(32 * p) * ldq +              \
-                                            ((k0) >= kwrap ? (k0) - kwrap : (k0)));     \
-  }
-#define NS_LSTORE(buf)                                                                 \
-  _Pragma("unroll") for (int p = 0; p < 8; ++p) {                                      \
-    bf16_t* sp = lds + (buf) * 2 * STAGE_ELEMS + (lrow + 32 * p) * LDS_STRIDE + lchunk; \
-    *reinterpret_cast<u32x4*>(sp) = rp[p];                                             \
-    *reinterpret_cast<u32x4*>(sp + STAGE_ELEMS) = rq[p];                               \
-  }
-  NS_GLOAD(0);
-  NS_LSTORE(0);
-  __syncthreads();
-  for (int kt = 0; kt < KT; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < KT) { NS_GLOAD((kt + 1) * NS_BK); }
-    const bf16_t* bp = lds + cur * 2 * STAGE_ELEMS + (wr * 128 + frow) * LDS_STRIDE + fk;
-    const bf16_t* bq = lds + cur * 2 * STAGE_ELEMS + STAGE_ELEMS + (wc * 128 + frow) * LDS_STRIDE + fk;
+  pipeline(
+      K / BK, lds,
+      [&](int kt) {
+        char* base = lds + (kt % STAGES) * STAGE_BYTES;
 #pragma unroll
-    for (int s = 0; s < NS_BK / 16; ++s) {
-      bf16x8 fa[4], fb[4];
+        for (int q = 0; q < LOADS; ++q)
+          __builtin_amdgcn_global_load_lds((const gbl_void_t*)(src[q] + kt * BK), (lds_void_t*)(base + dst_off[q]),
+                                           16, 0, 0);
+      },
+      [&](int buf, const char* st, int h) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        fa[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(bp + i * 32 * LDS_STRIDE + s * 16));
+        for (int i = 0; i < I; ++i) fa[buf][i] = *reinterpret_cast<const bf16x8*>(st + offa[i][h]);
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        fb[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(bq + j * 32 * LDS_STRIDE + s * 16));
+        for (int j = 0; j < J; ++j) fb[buf][j] = *reinterpret_cast<const bf16x8*>(st + offb[j][h]);
+      },
+      [&](int buf) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < I; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-    }
-    if (kt + 1 < KT) { NS_LSTORE(cur ^ 1); }
-    __syncthreads();
-  }
+          for (int j = 0; j < J; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[buf][i], fb[buf][j], acc[i][j], 0, 0, 0);
+      });
 
-#undef NS_GLOAD
-#undef NS_LSTORE
   // ---------------------------------------------------------------- epilogue
-  // Four rounds; round i stages rows {wr*128 + i*32 + [0,32)} of both wave rows
+  // Four rounds; round i stages rows {wr*TM + i*32 + [0,32)} of both wave rows
   // (64 tile rows x 256 cols, fp32) in LDS.  Pass 1 reads 8 consecutive
   // columns per thread, applies the phase's epilogue, writes bf16 rows and
-  // keeps the bf16 values in LDS; pass 2 writes the transposed orientation
-  // from there.  Local staged row lr maps to tile row (lr >> 5)*128 + i*32 + (lr & 31).
-  float* stf = reinterpret_cast<float*>(lds);                                  // [64][EPI_F]
-  bf16_t* stb = reinterpret_cast<bf16_t*>(lds) + 2 * 64 * EPI_F;               // [64][EPI_B]
-  bf16_t* stl = stb + 64 * EPI_B;                                              // [64][EPI_B] (split lo)
-  const bool sym = phase != PH_UPDATE;
-  const bool mirror = sym && (t.ti != t.tj);
-  const int dst = args.src ^ 1;
-  const bool last = args.last != 0;
-  const bool wo_is_x = !d.tall;            // W orientation = canonical for wide matrices
+  // keeps the bf16 values in LDS; pass 2 writes the mirrored tile from there.
+  // Staged row lr is tile row (lr >> 5) * TM + i * 32 + (lr & 31).
+  float* stf = reinterpret_cast<float*>(lds);                       // [64][EPI_F]
+  bf16_t* stb = reinterpret_cast<bf16_t*>(lds + 64 * EPI_F * 4);    // [64][EPI_B]
+  bf16_t* stl = stb + 64 * EPI_B;                                   // [64][EPI_B] (split low part)
+  const bool mirror = t.ti != t.tj;
   float sc = 1.f;
-  if (args.first) {
+  if (args.first && phase == PH_GRAM) {
     const float sig = (float)d.scal[SC_SIGMA];
-    sc = (phase == PH_GRAM) ? sig * sig : (phase == PH_UPDATE ? sig : 1.f);
+    sc = sig * sig;
   }
-  bf16_t* out_row;       // row-major destination (pitch ldo) or nullptr
-  bf16_t* out_tr;        // transposed destination (pitch ldt) or nullptr
-  int ldo, ldt;
-  // Split B: the low part bf16(v - hi) goes lo_off columns to the right.
+  // Split B': the low part bf16(v - hi) goes mp columns to the right.
   const int lo_off = (phase == PH_POLY && d.split) ? mp : 0;
-  if (phase == PH_GRAM || phase == PH_POLY) {
-    out_row = (phase == PH_GRAM) ? d.A : d.B;
-    out_tr = mirror ? out_row : nullptr;
-    ldo = ldt = lo_off ? 2 * mp : mp;
-  } else {
-    out_row = (!last || wo_is_x) ? d.X[dst] : nullptr;
-    out_tr = (!last || !wo_is_x) ? d.XT[dst] : nullptr;
-    ldo = np;
-    ldt = mp;
-  }
-  const bf16_t* addend = (phase == PH_POLY) ? d.A : (phase == PH_UPDATE ? d.X[args.src] : nullptr);
-  const int lda = (phase == PH_POLY) ? mp : np;
-  const float k_add = (phase == PH_POLY) ? args.b : args.a;
-  const float k_acc = (phase == PH_POLY) ? args.c : 1.f;
-  float o2 = 0.f, d2 = 0.f;
+  bf16_t* out = (phase == PH_GRAM) ? d.A : d.B;
+  const int ldo = lo_off ? 2 * mp : mp;
+  const bool poly = phase == PH_POLY;
 
-  // Pass-1 mapping: 32 threads per staged row (8 columns each), 8 row groups.
+  constexpr int P1ROWS = NT / 32;           // pass 1: 32 threads per staged row, 8 columns each
   const int p1c = (tid & 31) * 8, p1r = tid >> 5;
-  // Pass-2 mapping: 4 threads per output column (8 rows each), 64 columns per pass.
+  constexpr int P2COLS = NT / 4;            // pass 2: 4 threads per output column, 8 rows each
   const int p2c = tid >> 2, p2s = (tid & 3) * 8;
 
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    __syncthreads();   // previous round's readers are done with the stage
+  for (int i = 0; i < I; ++i) {
+    __syncthreads();   // the ring / previous round's readers are done with LDS
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < J; ++j)
 #pragma unroll
       for (int g = 0; g < 4; ++g)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int lr = wr * 32 + g * 8 + (lane >> 5) * 4 + e;
-          const int lc = wc * 128 + j * 32 + (lane & 31);
+          const int lc = wc * TN + j * 32 + (lane & 31);
           stf[lr * EPI_F + lc] = acc[i][j][4 * g + e];
         }
     __syncthreads();
-    // Pass 1: straight orientation.
-    for (int k = 0; k < 8; ++k) {
-      const int lr = p1r + 8 * k;
-      const int R = row0 + (lr >> 5) * 128 + i * 32 + (lr & 31);
+    for (int k = 0; k < 64 / P1ROWS; ++k) {
+      const int lr = p1r + P1ROWS * k;
+      const int R = row0 + (lr >> 5) * TM + i * 32 + (lr & 31);
       const int C = col0 + p1c;
       const float4 a0 = *reinterpret_cast<const float4*>(stf + lr * EPI_F + p1c);
       const float4 a1 = *reinterpret_cast<const float4*>(stf + lr * EPI_F + p1c + 4);
       float v[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
-      if (addend) {
-        const uint4 q = *reinterpret_cast<const uint4*>(addend + (size_t)R * lda + C);
+      if (poly) {
+        // B' = a I + b A + c A A^T with the same bf16 A the product used.
+        const uint4 q = *reinterpret_cast<const uint4*>(d.A + (size_t)R * mp + C);
         const uint32_t qw[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           const float av = bf2f_((bf16_t)((qw[e >> 1] >> (16 * (e & 1))) & 0xffffu));
-          v[e] = k_add * av + k_acc * v[e];
+          v[e] = args.b * av + args.c * v[e] + (R == C + e ? args.a : 0.f);
         }
       }
       uint32_t hw[4], lw[4];
@@ -226,66 +309,205 @@ __global__ __launch_bounds__(NTHREADS, 1) void ns_gemm_kernel(NsArgs args) {
           stl[lr * EPI_B + p1c + e] = l0;
           stl[lr * EPI_B + p1c + e + 1] = l1;
         }
-        if (last && phase == PH_UPDATE) {
-          // Canonical (R, C) is W(R, C) for wide, W(C, R) for tall matrices.
+      }
+      *reinterpret_cast<uint4*>(out + (size_t)R * ldo + C) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+      if (lo_off)
+        *reinterpret_cast<uint4*>(out + (size_t)R * ldo + lo_off + C) = make_uint4(lw[0], lw[1], lw[2], lw[3]);
+    }
+    if (mirror) {
+      __syncthreads();
 #pragma unroll
-          for (int u = 0; u < 2; ++u) {
-            const int cc = C + e + u;
-            if (R < d.mc && cc < d.nc) {
-              const float o = bf2f_(u ? h1 : h0);
-              const float dv = (d.tall ? d.Rv[R] * d.Lv[cc] : d.Lv[R] * d.Rv[cc]) * o;
+      for (int q = 0; q < NS_TILE / P2COLS; ++q) {
+        const int lc = p2c + P2COLS * q;
+        const int C = col0 + lc;
+#pragma unroll
+        for (int band = 0; band < 2; ++band) {
+          const int lr0 = band * 32 + p2s;
+          const int R = row0 + band * TM + i * 32 + p2s;
+          uint32_t hw[4];
+#pragma unroll
+          for (int e = 0; e < 8; e += 2)
+            hw[e >> 1] = (uint32_t)stb[(lr0 + e) * EPI_B + lc] | ((uint32_t)stb[(lr0 + e + 1) * EPI_B + lc] << 16);
+          *reinterpret_cast<uint4*>(out + (size_t)C * ldo + R) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+          if (lo_off) {
+#pragma unroll
+            for (int e = 0; e < 8; e += 2)
+              hw[e >> 1] = (uint32_t)stl[(lr0 + e) * EPI_B + lc] | ((uint32_t)stl[(lr0 + e + 1) * EPI_B + lc] << 16);
+            *reinterpret_cast<uint4*>(out + (size_t)C * ldo + lo_off + R) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+          }
+        }
+      }
+    }
+  }
+}
+
+// ===========================================================================
+// Update phase: X' = s B' X  (NN), computed as C^T = X^T B'^T blocks.
+// ===========================================================================
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void ns_update_kernel(NsArgs args) {
+  constexpr int NB = TM / 32;                // B' fragments (output rows, MFMA B operand)
+  constexpr int NA = TN / 32;                // X fragments (output cols, MFMA A operand)
+  constexpr int ROWS_PER_LOAD = 1024 / RB;   // B' rows per 1 KB load
+  constexpr int LOADS_P = NS_TILE / ROWS_PER_LOAD;
+  constexpr int KROWS_PER_LOAD = 1024 / KN_ROW;   // X k-rows per 1 KB load (2)
+
+  extern __shared__ __attribute__((aligned(16))) char lds[];
+  const Tile t = args.tiles[xcd_remap(blockIdx.x, gridDim.x)];
+  const MatDesc& d = args.desc[t.mat];
+  const int mp = d.mp, np = d.np;
+  // Split matrices contract over [B'_hi | B'_lo] and [X ; X]: K = 2 mp.
+  const int ldb = d.split ? 2 * mp : mp;
+  const int K = ldb;
+  const bf16_t* Bm = d.B;
+  const bf16_t* X = d.X[args.src];
+  const int row0 = t.ti * NS_TILE, col0 = t.tj * NS_TILE;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wr = wave / 4, wc = wave % 4;
+
+  const bf16_t* src[LOADS];
+  int dst_off[LOADS];
+  bool isx[LOADS];
+#pragma unroll
+  for (int q = 0; q < LOADS; ++q) {
+    const int g = wave + q * NW;
+    if (g < LOADS_P) {
+      const int row = g * ROWS_PER_LOAD + lane / CPR;
+      const int kc = (lane % CPR) ^ ((row / RPP) % CPR);
+      src[q] = Bm + (size_t)(row0 + row) * ldb + kc * 8;
+      dst_off[q] = g * 1024;
+      isx[q] = false;
+    } else {
+      const int qi = g - LOADS_P;
+      const int k = qi * KROWS_PER_LOAD + lane / 32;
+      const int c = (lane % 32) ^ (4 * (k & 3));   // logical 16-byte chunk of this physical slot
+      src[q] = X + (size_t)k * np + col0 + c * 8;
+      dst_off[q] = OPER_BYTES + qi * 1024;
+      isx[q] = true;
+    }
+  }
+  // B' fragments: rows of the output, k contiguous.
+  int offb[NB][H];
+#pragma unroll
+  for (int h = 0; h < H; ++h)
+#pragma unroll
+    for (int b = 0; b < NB; ++b) offb[b][h] = swz_rk(wr * TM + b * 32 + (lane & 31), 2 * h + (lane >> 5));
+  // X fragments through transposed reads: in each 16-lane group, lane
+  // j = q + 4r addresses row k0 + r, columns n0 + 4q .. n0 + 4q + 3; the
+  // read hands lane i the four rows of column n0 + i.
+  int offx[NA][2];
+  {
+    const int r = (lane & 15) >> 2, q = lane & 3;
+#pragma unroll
+    for (int a = 0; a < NA; ++a)
+#pragma unroll
+      for (int r2 = 0; r2 < 2; ++r2) {
+        const int k = 8 * (lane >> 5) + 4 * r2 + r;
+        const int n = wc * TN + a * 32 + 16 * ((lane >> 4) & 1) + 4 * q;
+        offx[a][r2] = OPER_BYTES + swz_kn(k, n);
+      }
+  }
+
+  f32x16 acc[NA][NB];
+#pragma unroll
+  for (int a = 0; a < NA; ++a)
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.f;
+  bf16x8 fx[2][NA], fb[2][NB];
+
+  pipeline(
+      K / BK, lds,
+      [&](int kt) {
+        const int k0 = kt * BK;
+        const int k0x = k0 >= mp ? k0 - mp : k0;   // X's k wraps for split matrices
+        char* base = lds + (kt % STAGES) * STAGE_BYTES;
+#pragma unroll
+        for (int q = 0; q < LOADS; ++q)
+          __builtin_amdgcn_global_load_lds(
+              (const gbl_void_t*)(isx[q] ? src[q] + (size_t)k0x * np : src[q] + k0),
+              (lds_void_t*)(base + dst_off[q]), 16, 0, 0);
+      },
+      [&](int buf, const char* st, int h) {
+#pragma unroll
+        for (int b = 0; b < NB; ++b) fb[buf][b] = *reinterpret_cast<const bf16x8*>(st + offb[b][h]);
+#pragma unroll
+        for (int a = 0; a < NA; ++a) {
+          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_i16x4_t*)(st + offx[a][0] + h * 16 * KN_ROW));
+          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_i16x4_t*)(st + offx[a][1] + h * 16 * KN_ROW));
+          fx[buf][a] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        }
+      },
+      [&](int buf) {
+#pragma unroll
+        for (int a = 0; a < NA; ++a)
+#pragma unroll
+          for (int b = 0; b < NB; ++b)
+            acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fx[buf][a], fb[buf][b], acc[a][b], 0, 0, 0);
+      });
+
+  // ---------------------------------------------------------------- epilogue
+  // acc[a][b][4g + e] = C(m, n + e), m = row0 + wr*TM + b*32 + (lane & 31),
+  // n = col0 + wc*TN + a*32 + 8g + 4*(lane >> 5): four consecutive bf16 per store.
+  const float sc = args.first ? (float)d.scal[SC_SIGMA] : 1.f;
+  bf16_t* Xn = d.X[args.src ^ 1];
+  const bool last = args.last != 0;
+  float o2 = 0.f, d2 = 0.f;
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    const int m = row0 + wr * TM + b * 32 + (lane & 31);
+    // Canonical (m, n) is W(m, n) for wide and W(n, m) for tall matrices.
+    const float lm = (last && m < d.mc) ? (d.tall ? d.Rv[m] : d.Lv[m]) : 0.f;
+#pragma unroll
+    for (int a = 0; a < NA; ++a) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int n = col0 + wc * TN + a * 32 + 8 * g + 4 * (lane >> 5);
+        bf16_t hv[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) hv[e] = f2bf_rne(sc * acc[a][b][4 * g + e]);
+        uint2 pk;
+        pk.x = (uint32_t)hv[0] | ((uint32_t)hv[1] << 16);
+        pk.y = (uint32_t)hv[2] | ((uint32_t)hv[3] << 16);
+        *reinterpret_cast<uint2*>(Xn + (size_t)m * np + n) = pk;
+        if (last && m < d.mc) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (n + e < d.nc) {
+              const float o = bf2f_(hv[e]);
+              const float dv = lm * o * (d.tall ? d.Lv[n + e] : d.Rv[n + e]);
               o2 += o * o;
               d2 += dv * dv;
             }
           }
         }
       }
-      if (out_row) {
-        *reinterpret_cast<uint4*>(out_row + (size_t)R * ldo + C) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
-        if (lo_off)
-          *reinterpret_cast<uint4*>(out_row + (size_t)R * ldo + lo_off + C) = make_uint4(lw[0], lw[1], lw[2], lw[3]);
-      }
-    }
-    if (out_tr) {
-      __syncthreads();
-      // Pass 2: transposed orientation, out_tr[C][R .. R+7] for both row bands.
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int lc = p2c + 64 * q;
-        const int C = col0 + lc;
-#pragma unroll
-        for (int band = 0; band < 2; ++band) {
-          const int lr0 = band * 32 + p2s;
-          const int R = row0 + band * 128 + i * 32 + p2s;
-          uint32_t hw[4];
-#pragma unroll
-          for (int e = 0; e < 8; e += 2)
-            hw[e >> 1] = (uint32_t)stb[(lr0 + e) * EPI_B + lc] | ((uint32_t)stb[(lr0 + e + 1) * EPI_B + lc] << 16);
-          *reinterpret_cast<uint4*>(out_tr + (size_t)C * ldt + R) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
-          if (lo_off) {
-#pragma unroll
-            for (int e = 0; e < 8; e += 2)
-              hw[e >> 1] = (uint32_t)stl[(lr0 + e) * EPI_B + lc] | ((uint32_t)stl[(lr0 + e + 1) * EPI_B + lc] << 16);
-            *reinterpret_cast<uint4*>(out_tr + (size_t)C * ldt + lo_off + R) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
-          }
-        }
-      }
     }
   }
-  if (phase == PH_UPDATE && last) {
+  if (last) {
     // Deterministic per-tile sums for the graft norms.
     __syncthreads();
-    float* red = stf;
+    float* red = reinterpret_cast<float*>(lds);
     o2 = wsum(o2);
     d2 = wsum(d2);
     if (lane == 0) {
       red[wave] = o2;
-      red[4 + wave] = d2;
+      red[NW + wave] = d2;
     }
     __syncthreads();
     if (tid == 0) {
-      d.gpart[2 * (size_t)t.idx + 0] = (red[0] + red[1]) + (red[2] + red[3]);
-      d.gpart[2 * (size_t)t.idx + 1] = (red[4] + red[5]) + (red[6] + red[7]);
+      float so = 0.f, sd = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) {
+        so += red[w];
+        sd += red[NW + w];
+      }
+      d.gpart[2 * (size_t)t.idx + 0] = so;
+      d.gpart[2 * (size_t)t.idx + 1] = sd;
     }
   }
 }
@@ -294,12 +516,16 @@ hipError_t launch_ns_gemm(const NsArgs& a, hipStream_t s) {
   if (a.ntiles == 0) return hipSuccess;
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&ns_gemm_kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
-    if (e != hipSuccess) return e;
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&ns_gemm_sym_kernel),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
+    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&ns_update_kernel),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
     attr_set = true;
   }
-  hipLaunchKernelGGL(ns_gemm_kernel, dim3(a.ntiles), dim3(NTHREADS), LDS_BYTES, s, a);
+  if (a.phase == PH_UPDATE)
+    hipLaunchKernelGGL(ns_update_kernel, dim3(a.ntiles), dim3(NT), LDS_BYTES, s, a);
+  else
+    hipLaunchKernelGGL(ns_gemm_sym_kernel, dim3(a.ntiles), dim3(NT), LDS_BYTES, s, a);
   return hipGetLastError();
 }
 

@@ -52,7 +52,7 @@ class malt_state_layout_t(ctypes.Structure):
 
 class malt_debug_layout_t(ctypes.Structure):
     _fields_ = [("Lv", c_int64), ("Rv", c_int64), ("O", c_int64), ("X0", c_int64),
-                ("scalars", c_int64), ("O_pitch", c_int64)]
+                ("scalars", c_int64), ("O_pitch", c_int64), ("O_transposed", c_int64)]
 
 
 class malt_profile_t(ctypes.Structure):
@@ -225,11 +225,13 @@ class Plan:
         L = self.debug_layout(i)
         m, n = self.shapes[i]
         w = self.workspace
-        rows_alloc = -(-m // 256) * 256
+        mc, nc = min(m, n), max(m, n)
+        rows_alloc = -(-mc // 256) * 256
 
         def bf16(off):
-            return w[off: off + 2 * rows_alloc * L.O_pitch].view(torch.bfloat16).view(
-                rows_alloc, L.O_pitch)[:m, :n]
+            canon = w[off: off + 2 * rows_alloc * L.O_pitch].view(torch.bfloat16).view(
+                rows_alloc, L.O_pitch)[:mc, :nc]
+            return canon.t() if L.O_transposed else canon
 
         sc = w[L.scalars: L.scalars + 8 * 16].view(torch.float64)
         return {"Lv": w[L.Lv: L.Lv + 4 * m].view(torch.float32),
