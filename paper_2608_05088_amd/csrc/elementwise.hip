@@ -24,14 +24,6 @@ __device__ __forceinline__ double wave_sum_d(double v) {
   return v;
 }
 
-// Round-to-nearest-even float -> bf16 bits (NaN stays NaN).
-__device__ __forceinline__ bf16_t f2bf(float x) {
-  uint32_t u = __float_as_uint(x);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
-}
-
 __device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
 // Load 4 consecutive floats of one row starting at column c (columns >= n read 0).
@@ -171,17 +163,16 @@ __global__ __launch_bounds__(NTHREADS) void scale_convert_kernel(EwArgs a) {
         }
       }
     }
-    bf16_t h[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) h[e] = f2bf(x[e]);
+    uint2 pk;
+    pk.x = pack_bf16x2(x[0], x[1]);
+    pk.y = pack_bf16x2(x[2], x[3]);
     if (!d.tall) {
-      uint2 pk;
-      pk.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
-      pk.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
       *reinterpret_cast<uint2*>(X0 + (size_t)r * ldx + c0 + cc) = pk;
     } else {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) tsh[rr][cc + e] = h[e];
+      tsh[rr][cc + 0] = (bf16_t)(pk.x & 0xffffu);
+      tsh[rr][cc + 1] = (bf16_t)(pk.x >> 16);
+      tsh[rr][cc + 2] = (bf16_t)(pk.y & 0xffffu);
+      tsh[rr][cc + 3] = (bf16_t)(pk.y >> 16);
     }
   }
   if (d.tall) {

@@ -24,6 +24,18 @@ constexpr int NTHREADS = 256;
 
 typedef uint16_t bf16_t;   // bf16 storage
 
+typedef float malt_f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 malt_bf16x2 __attribute__((ext_vector_type(2)));
+
+// Two floats -> two bf16 (round to nearest even; one v_cvt_pk_bf16_f32),
+// packed low | high << 16.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const malt_f32x2 v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, malt_bf16x2));
+}
+__device__ __forceinline__ float bf16_lo(uint32_t p) { return __uint_as_float(p << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t p) { return __uint_as_float(p & 0xffff0000u); }
+
 // Per-matrix scalar slots (float64) in the workspace.
 enum {
   SC_S = 0,       // ||L M R||_F

@@ -71,12 +71,6 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4_t;
 typedef __attribute__((address_space(1))) void gbl_void_t;
 
-__device__ __forceinline__ bf16_t f2bf_rne(float x) {
-  uint32_t u = __float_as_uint(x);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
-}
 __device__ __forceinline__ float bf2f_(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
 __device__ __forceinline__ float wsum(float v) {
@@ -171,11 +165,17 @@ void ns_gemm_sym_kernel(NsArgs args) {
   constexpr int LOADS_PER_OPER = NS_TILE / ROWS_PER_LOAD;
 
   extern __shared__ __attribute__((aligned(16))) char lds[];
+  // Every descriptor field the tile needs is read here, before any store, so
+  // the uniform loads go through the scalar cache.
   const Tile t = args.tiles[xcd_remap(blockIdx.x, gridDim.x)];
-  const MatDesc& d = args.desc[t.mat];
+  const MatDesc* __restrict__ d = args.desc + t.mat;
   const int phase = args.phase;
-  const int mp = d.mp, np = d.np;
-  const bf16_t* P = (phase == PH_GRAM) ? d.X[args.src] : d.A;
+  const int mp = d->mp, np = d->np;
+  const bool split = d->split != 0;
+  bf16_t* const Am = d->A;
+  bf16_t* const Bm = d->B;
+  const bf16_t* P = (phase == PH_GRAM) ? d->X[args.src] : Am;
+  const float sig = (args.first && phase == PH_GRAM) ? (float)d->scal[SC_SIGMA] : 1.f;
   const int ld = (phase == PH_GRAM) ? np : mp;
   const int K = ld;
   const int row0 = t.ti * NS_TILE, col0 = t.tj * NS_TILE;
@@ -248,14 +248,10 @@ void ns_gemm_sym_kernel(NsArgs args) {
   bf16_t* stb = reinterpret_cast<bf16_t*>(lds + 64 * EPI_F * 4);    // [64][EPI_B]
   bf16_t* stl = stb + 64 * EPI_B;                                   // [64][EPI_B] (split low part)
   const bool mirror = t.ti != t.tj;
-  float sc = 1.f;
-  if (args.first && phase == PH_GRAM) {
-    const float sig = (float)d.scal[SC_SIGMA];
-    sc = sig * sig;
-  }
+  const float sc = sig * sig;
   // Split B': the low part bf16(v - hi) goes mp columns to the right.
-  const int lo_off = (phase == PH_POLY && d.split) ? mp : 0;
-  bf16_t* out = (phase == PH_GRAM) ? d.A : d.B;
+  const int lo_off = (phase == PH_POLY && split) ? mp : 0;
+  bf16_t* out = (phase == PH_GRAM) ? Am : Bm;
   const int ldo = lo_off ? 2 * mp : mp;
   const bool poly = phase == PH_POLY;
 
@@ -287,7 +283,7 @@ void ns_gemm_sym_kernel(NsArgs args) {
       float v[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
       if (poly) {
         // B' = a I + b A + c A A^T with the same bf16 A the product used.
-        const uint4 q = *reinterpret_cast<const uint4*>(d.A + (size_t)R * mp + C);
+        const uint4 q = *reinterpret_cast<const uint4*>(Am + (size_t)R * mp + C);
         const uint32_t qw[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
@@ -299,15 +295,15 @@ void ns_gemm_sym_kernel(NsArgs args) {
 #pragma unroll
       for (int e = 0; e < 8; e += 2) {
         const float v0 = sc * v[e], v1 = sc * v[e + 1];
-        const bf16_t h0 = f2bf_rne(v0), h1 = f2bf_rne(v1);
-        hw[e >> 1] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-        stb[lr * EPI_B + p1c + e] = h0;
-        stb[lr * EPI_B + p1c + e + 1] = h1;
+        const uint32_t hp = pack_bf16x2(v0, v1);
+        hw[e >> 1] = hp;
+        stb[lr * EPI_B + p1c + e] = (bf16_t)(hp & 0xffffu);
+        stb[lr * EPI_B + p1c + e + 1] = (bf16_t)(hp >> 16);
         if (lo_off) {
-          const bf16_t l0 = f2bf_rne(v0 - bf2f_(h0)), l1 = f2bf_rne(v1 - bf2f_(h1));
-          lw[e >> 1] = (uint32_t)l0 | ((uint32_t)l1 << 16);
-          stl[lr * EPI_B + p1c + e] = l0;
-          stl[lr * EPI_B + p1c + e + 1] = l1;
+          const uint32_t lp = pack_bf16x2(v0 - bf16_lo(hp), v1 - bf16_hi(hp));
+          lw[e >> 1] = lp;
+          stl[lr * EPI_B + p1c + e] = (bf16_t)(lp & 0xffffu);
+          stl[lr * EPI_B + p1c + e + 1] = (bf16_t)(lp >> 16);
         }
       }
       *reinterpret_cast<uint4*>(out + (size_t)R * ldo + C) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
@@ -353,14 +349,22 @@ void ns_update_kernel(NsArgs args) {
   constexpr int KROWS_PER_LOAD = 1024 / KN_ROW;   // X k-rows per 1 KB load (2)
 
   extern __shared__ __attribute__((aligned(16))) char lds[];
+  // Every descriptor field the tile needs is read here, before any store, so
+  // the uniform loads go through the scalar cache.
   const Tile t = args.tiles[xcd_remap(blockIdx.x, gridDim.x)];
-  const MatDesc& d = args.desc[t.mat];
-  const int mp = d.mp, np = d.np;
+  const MatDesc* __restrict__ d = args.desc + t.mat;
+  const int mp = d->mp, np = d->np, mc = d->mc, nc = d->nc;
+  const bool tall = d->tall != 0;
   // Split matrices contract over [B'_hi | B'_lo] and [X ; X]: K = 2 mp.
-  const int ldb = d.split ? 2 * mp : mp;
+  const int ldb = d->split ? 2 * mp : mp;
   const int K = ldb;
-  const bf16_t* Bm = d.B;
-  const bf16_t* X = d.X[args.src];
+  const bf16_t* Bm = d->B;
+  const bf16_t* X = d->X[args.src];
+  bf16_t* const Xn = d->X[args.src ^ 1];
+  const float* const Lv = d->Lv;
+  const float* const Rv = d->Rv;
+  float* const gpart = d->gpart;
+  const float sc = args.first ? (float)d->scal[SC_SIGMA] : 1.f;
   const int row0 = t.ti * NS_TILE, col0 = t.tj * NS_TILE;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -453,62 +457,89 @@ void ns_update_kernel(NsArgs args) {
   // ---------------------------------------------------------------- epilogue
   // acc[a][b][4g + e] = C(m, n + e), m = row0 + wr*TM + b*32 + (lane & 31),
   // n = col0 + wc*TN + a*32 + 8g + 4*(lane >> 5): four consecutive bf16 per store.
-  const float sc = args.first ? (float)d.scal[SC_SIGMA] : 1.f;
-  bf16_t* Xn = d.X[args.src ^ 1];
-  const bool last = args.last != 0;
-  float o2 = 0.f, d2 = 0.f;
+  const int mlane = row0 + wr * TM + (lane & 31);
+  const int nlane = col0 + wc * TN + 4 * (lane >> 5);
+  if (!args.last) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+#pragma unroll
+      for (int a = 0; a < NA; ++a)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          uint2 pk;
+          pk.x = pack_bf16x2(sc * acc[a][b][4 * g + 0], sc * acc[a][b][4 * g + 1]);
+          pk.y = pack_bf16x2(sc * acc[a][b][4 * g + 2], sc * acc[a][b][4 * g + 3]);
+          *reinterpret_cast<uint2*>(Xn + (size_t)(mlane + b * 32) * np + nlane + a * 32 + 8 * g) = pk;
+        }
+    return;
+  }
+  // Last iteration: also the per-tile sums of O^2 and (L O R)^2.  Canonical
+  // (m, n) is W(m, n) for wide and W(n, m) for tall matrices.
+  const float* const Lm = tall ? Rv : Lv;   // factor indexed by the canonical row
+  const float* const Ln = tall ? Lv : Rv;   // factor indexed by the canonical column
+  // (Lm O Ln)^2 = Lm^2 Ln^2 O^2: four squared row factors per lane, four
+  // squared column factors per (a, g).
+  float lm2[NB];
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
-    const int m = row0 + wr * TM + b * 32 + (lane & 31);
-    // Canonical (m, n) is W(m, n) for wide and W(n, m) for tall matrices.
-    const float lm = (last && m < d.mc) ? (d.tall ? d.Rv[m] : d.Lv[m]) : 0.f;
+    const int m = mlane + b * 32;
+    const float l = m < mc ? Lm[m] : 0.f;
+    lm2[b] = l * l;
+  }
+  float o2 = 0.f, d2 = 0.f;
 #pragma unroll
-    for (int a = 0; a < NA; ++a) {
+  for (int a = 0; a < NA; ++a) {
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int n = col0 + wc * TN + a * 32 + 8 * g + 4 * (lane >> 5);
-        bf16_t hv[4];
+    for (int g = 0; g < 4; ++g) {
+      const int n = nlane + a * 32 + 8 * g;
+      float ln2[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) hv[e] = f2bf_rne(sc * acc[a][b][4 * g + e]);
+      for (int e = 0; e < 4; ++e) {
+        const float l = n + e < nc ? Ln[n + e] : 0.f;
+        ln2[e] = l * l;
+      }
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const int m = mlane + b * 32;
         uint2 pk;
-        pk.x = (uint32_t)hv[0] | ((uint32_t)hv[1] << 16);
-        pk.y = (uint32_t)hv[2] | ((uint32_t)hv[3] << 16);
+        pk.x = pack_bf16x2(sc * acc[a][b][4 * g + 0], sc * acc[a][b][4 * g + 1]);
+        pk.y = pack_bf16x2(sc * acc[a][b][4 * g + 2], sc * acc[a][b][4 * g + 3]);
         *reinterpret_cast<uint2*>(Xn + (size_t)m * np + n) = pk;
-        if (last && m < d.mc) {
+        const float ov[4] = {bf16_lo(pk.x), bf16_hi(pk.x), bf16_lo(pk.y), bf16_hi(pk.y)};
+        float rowo = 0.f, rowd = 0.f;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            if (n + e < d.nc) {
-              const float o = bf2f_(hv[e]);
-              const float dv = lm * o * (d.tall ? d.Lv[n + e] : d.Rv[n + e]);
-              o2 += o * o;
-              d2 += dv * dv;
-            }
-          }
+        for (int e = 0; e < 4; ++e) {
+          const float q = (n + e < nc) ? ov[e] * ov[e] : 0.f;   // zero padding contributes 0 anyway
+          rowo += q;
+          rowd += ln2[e] * q;
+        }
+        if (m < mc) {
+          o2 += rowo;
+          d2 += lm2[b] * rowd;
         }
       }
+      asm volatile("" ::: "memory");   // keep the column-factor loads of one (a, g) at a time
     }
   }
-  if (last) {
-    // Deterministic per-tile sums for the graft norms.
-    __syncthreads();
-    float* red = reinterpret_cast<float*>(lds);
-    o2 = wsum(o2);
-    d2 = wsum(d2);
-    if (lane == 0) {
-      red[wave] = o2;
-      red[NW + wave] = d2;
-    }
-    __syncthreads();
-    if (tid == 0) {
-      float so = 0.f, sd = 0.f;
+  // Deterministic per-tile sums for the graft norms.
+  __syncthreads();
+  float* red = reinterpret_cast<float*>(lds);
+  o2 = wsum(o2);
+  d2 = wsum(d2);
+  if (lane == 0) {
+    red[wave] = o2;
+    red[NW + wave] = d2;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    float so = 0.f, sd = 0.f;
 #pragma unroll
-      for (int w = 0; w < NW; ++w) {
-        so += red[w];
-        sd += red[NW + w];
-      }
-      d.gpart[2 * (size_t)t.idx + 0] = so;
-      d.gpart[2 * (size_t)t.idx + 1] = sd;
+    for (int w = 0; w < NW; ++w) {
+      so += red[w];
+      sd += red[NW + w];
     }
+    gpart[2 * (size_t)t.idx + 0] = so;
+    gpart[2 * (size_t)t.idx + 1] = sd;
   }
 }
 

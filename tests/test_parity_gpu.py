@@ -186,3 +186,30 @@ def test_graft_identity_on_gpu_scalars():
         assert abs(np.sqrt(g[0].scal[k]["d2"]) - nD) / nD < 1e-5
         expect = w.lr * g[0].scal[k]["alpha"] * nO * nD / (nD + 1e-8)
         assert abs(np.linalg.norm(g[0].dW[k]) - expect) / expect < 1e-3
+
+
+def _bf16_rne(x32):
+    """float32 -> bf16 bit patterns, round to nearest even (NaN-free input)."""
+    u = np.asarray(x32, np.float32).view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+def test_scale_convert_is_bitexact_rne():
+    # X0 = bf16((L_i * M_ij) * R_j) in float32, exactly as a host RNE of the same
+    # float32 product of the GPU's own L, M, R (byte-exact work).
+    import torch
+    shapes = [(200, 520), (520, 200), (33, 47)]
+    say(f"[parity] bf16 conversion bit-exact {shapes}")
+    W0 = [wl.weight(99, i, s) for i, s in enumerate(shapes)]
+    G = [wl.grad(99, 1, i, s, "student_t3") for i, s in enumerate(shapes)]
+    plan = lm.Plan(shapes, "malt")
+    Wd, Gd = to_dev(W0), to_dev(G)
+    plan.step(Wd, Gd, lm.make_hparams(lr=1e-2, ns_steps=1))
+    torch.cuda.synchronize()
+    for i, (m, n) in enumerate(shapes):
+        M = plan.state_views(i)[0].cpu().numpy()
+        dv = plan.debug_views(i)
+        Lv, Rv = dv["Lv"].cpu().numpy(), dv["Rv"].cpu().numpy()
+        x = (Lv[:, None].astype(np.float32) * M) * Rv[None, :].astype(np.float32)
+        got = dv["X0"].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+        assert np.array_equal(got, _bf16_rne(x)), f"matrix {i}: bf16 conversion differs from RNE"
