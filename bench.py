@@ -25,6 +25,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 matrix-core peak
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ns_update_gpt2_large_traffic.md")
+NS_SOURCE = os.path.join(ROOT, "paper_2608_05088_amd", "csrc", "ns_gemm.hip")
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
 METRIC = "MALT step latency (ms) per GPT-2 param set; NS MFMA % bf16 peak; HBM GB/s"
 
@@ -40,6 +42,23 @@ def parse():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run one plain 1 GiB device-to-device copy (HBM counter calibration)")
     return ap.parse_args()
+
+
+def recorded_traffic(workload: str):
+    """HBM bytes per ns_update_kernel launch from the committed PMC summary, or
+    None when the summary is for another workload or an older kernel source."""
+    import hashlib
+    if workload != "gpt2_large" or not os.path.exists(TRAFFIC_FILE):
+        return None
+    fields = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            fields[k.strip().lstrip("- ").strip("`")] = v.strip().strip("`")
+    sha = hashlib.sha256(open(NS_SOURCE, "rb").read()).hexdigest()
+    if fields.get("source_sha256") != sha or "traffic_bytes_per_launch" not in fields:
+        return None
+    return float(fields["traffic_bytes_per_launch"])
 
 
 def cpu_baseline(w, layers: int):
@@ -156,16 +175,22 @@ def main():
         kernels[name] = ent
     ns = [prof[k] for k in ("ns_gram", "ns_poly", "ns_update")]
     ns_ms = sum(v["ms"] for v in ns)
-    ns_launches = sum(v["launches"] for v in ns)
     ns_flops_step = sum(v["flops"] for v in ns)
-    flops_per_launch = ns_flops_step * K / ns_launches
-    avg_launch_s = ns_ms * 1e-3 / ns_launches
+    # Dominant kernel: the Newton-Schulz update product B'X (ns_update_kernel).
+    upd = prof["ns_update"]
+    flops_per_launch = upd["flops"] * K / upd["launches"]
+    avg_launch_s = upd["ms"] * 1e-3 / upd["launches"]
     achieved = flops_per_launch / avg_launch_s / 1e12
-    roofline = {"bound": "mfma", "kernel": "ns_gemm_kernel (Gram, polynomial and update phases)",
+    roofline = {"bound": "mfma", "kernel": "ns_update_kernel (Newton-Schulz X' = B'X, all matrices)",
                 "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": recorded_traffic(w.name),
                 "flops_per_launch": flops_per_launch, "avg_launch_ms": round(avg_launch_s * 1e3, 4),
-                "flops_basis": "symmetric minimum: m'^2 n' (Gram) + m'^3 (A^2) + 2 m'^2 n' (B X) per NS iteration"}
+                "flops_basis": "2 m'^2 n' per matrix per launch (B'X)"}
+    ns_all = {"kernels": "ns_gemm_sym_kernel + ns_update_kernel", "ms_per_step": round(ns_ms / K, 4),
+              "TFLOP_per_s": round(ns_flops_step * K / (ns_ms * 1e-3) / 1e12, 1),
+              "frac": round(ns_flops_step * K / (ns_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+              "flops_per_step": ns_flops_step,
+              "flops_basis": "symmetric minimum 3 m'^2 n' + m'^3 per matrix per NS iteration"}
     ew_bytes = sum(prof[k]["bytes"] for k in ("momentum_rowcol", "scale_convert", "backmap_write"))
     ew_ms = sum(prof[k]["ms"] for k in ("momentum_rowcol", "scale_convert", "backmap_write")) / K
     hbm = {"elementwise_GB_per_s": round(ew_bytes / (ew_ms * 1e-3) / 1e9, 1),
@@ -175,10 +200,11 @@ def main():
     del grad_sets, Wd
     torch.cuda.empty_cache()
     if args.copy_calibration:
-        # A plain copy of known size: 2^30 bytes read, 2^30 bytes written.
+        # A plain copy kernel of known size (an elementwise x*1 kernel, not the
+        # SDMA engine): 2^30 bytes read, 2^30 bytes written.
         src = torch.ones(2 ** 28, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
-        dst.copy_(src)
+        torch.mul(src, 1.0, out=dst)
         torch.cuda.synchronize()
         del src, dst
 
@@ -192,7 +218,8 @@ def main():
             "scaling": "weak", "vs_baseline": None, "dtype": "bf16+fp32", "data": "synthetic",
             "config": {"workload": w.name, "variant": w.variant, "matrices": len(shapes), "params": w.numel,
                        "lr": w.lr, "grad_dist": w.dist, "timed": f"{K} consecutive steps, persistent state"},
-            "roofline": roofline, "hbm": hbm, "kernels": kernels, "cpu_baseline": cpu}
+            "roofline": roofline, "newton_schulz": ns_all, "hbm": hbm, "kernels": kernels,
+            "cpu_baseline": cpu}
     print(json.dumps(line), flush=True)
 
 
