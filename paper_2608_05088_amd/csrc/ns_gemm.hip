@@ -101,6 +101,23 @@ __device__ __forceinline__ void wait_vm_c() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
+// One 16-byte-per-lane direct load into LDS at the wave-uniform address
+// lds_addr (lane i writes lds_addr + 16 i).  Issued from inline assembly so the
+// compiler does not track it: it cannot tell the ring slot being filled from
+// the slot being read, and before the transposed reads of the update it would
+// wait for each stage's loads right after issuing them.  Completion is ordered
+// by the pipeline's explicit vmcnt waits and barriers; m0 carries the LDS
+// address and needs one wait state after its write.
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds_addr) {
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(g), "{m0}"(lds_addr) : "memory");
+}
+
+// LDS byte address of a generic pointer into LDS: its low 32 bits (the flat
+// LDS aperture keeps the offset there), read as wave-uniform.
+__device__ __forceinline__ uint32_t lds_u32(const void* p) {
+  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)p);
+}
+
 // [row][k] tile (NT operands): 256 rows x BK bf16, CPR 16-byte chunks per row,
 // chunk kc stored at kc ^ ((row / RPP) % CPR): the ds_read_b128 fragment reads
 // of 16 consecutive rows at one chunk hit 16 distinct 4-bank groups.
@@ -430,9 +447,7 @@ void ns_update_kernel(NsArgs args) {
         char* base = lds + (kt % STAGES) * STAGE_BYTES;
 #pragma unroll
         for (int q = 0; q < LOADS; ++q)
-          __builtin_amdgcn_global_load_lds(
-              (const gbl_void_t*)(isx[q] ? src[q] + (size_t)k0x * np : src[q] + k0),
-              (lds_void_t*)(base + dst_off[q]), 16, 0, 0);
+          dma16(isx[q] ? src[q] + (size_t)k0x * np : src[q] + k0, lds_u32(base + dst_off[q]));
       },
       [&](int buf, const char* st, int h) {
 #pragma unroll

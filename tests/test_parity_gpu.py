@@ -213,3 +213,34 @@ def test_scale_convert_is_bitexact_rne():
         x = (Lv[:, None].astype(np.float32) * M) * Rv[None, :].astype(np.float32)
         got = dv["X0"].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
         assert np.array_equal(got, _bf16_rne(x)), f"matrix {i}: bf16 conversion differs from RNE"
+
+
+# Four shape kinds (a split contraction with K = 2 m', unsplit K = 768, a tall
+# matrix, a wide split one) repeated: 496 update tiles, more than one per
+# compute unit, of different K and pitch in one grouped launch.
+MIXED = [(100, 2900), (700, 1500), (1500, 300), (64, 5000)] * 8
+
+
+def test_many_tiles_mixed_shapes():
+    say(f"[parity] mixed shapes {len(MIXED)} matrices malter x2")
+    W0 = [wl.weight(96, i, s) for i, s in enumerate(MIXED)]
+    grads = [[wl.grad(96, t, i, s, "row_loguniform") for i, s in enumerate(MIXED)] for t in (1, 2)]
+    hp = dict(lr=4e-3)
+    g = run_gpu(MIXED, "malter", W0, grads, hp)
+    o = run_oracle(MIXED, "malter", W0, grads, hp)
+    worst = compare(g, o, "malter", label="mixed")
+    say(f"[parity] mixed worst {worst}")
+
+
+def test_c4_gpt2_large_sampled():
+    # The benchmark's launch configuration: all 144 GPT-2 Large matrices in one
+    # plan; the oracle checks one matrix of each shape from the first and last
+    # blocks (the step is independent per matrix).
+    w = wl.WORKLOADS[4]
+    sample = [0, 1, 2, 3, 140, 141, 142, 143]
+    say(f"[parity] C4 gpt2-large {len(w.shapes)} matrices {w.variant} x1, oracle on {sample}")
+    W0, grads = _inputs(w, 1)
+    g = run_gpu(list(w.shapes), w.variant, W0, grads, _hp(w), collect=sample)
+    o = run_oracle(list(w.shapes), w.variant, W0, grads, _hp(w), collect=sample)
+    worst = compare(g, o, w.variant, label="C4")
+    say(f"[parity] C4 worst {worst}")
