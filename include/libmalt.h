@@ -25,8 +25,9 @@
  * accumulation; everything else is fp32 with fp64 scalar combines.
  *
  * Conventions shared by every entry point
- *  - Matrices are dense, row-major float32, `rows x cols`, 1 <= rows, cols and
- *    rows*cols < 2^31.  Device pointers must be 4-byte aligned; rows whose
+ *  - Matrices are dense, row-major float32, `rows x cols`, 1 <= rows, cols <= 2^20,
+ *    min(rows, cols) <= 32768 and rows*cols < 2^31, also with both dimensions
+ *    rounded up to multiples of 256.  Device pointers must be 4-byte aligned; rows whose
  *    start is 16-byte aligned with cols % 4 == 0 take a vectorised path.
  *  - All device memory is owned by the caller.  The library never allocates
  *    device memory (it allocates a little pinned host memory at init).

@@ -70,9 +70,13 @@ malt_status_t check_shapes(const malt_shape_t* shapes, int32_t n) {
     const int64_t m = shapes[i].rows, c = shapes[i].cols;
     if (m < 1 || c < 1) return fail(MALT_ERR_SHAPE, "matrix %d: rows/cols must be >= 1 (got %lld x %lld)",
                                     i, (long long)m, (long long)c);
-    if (m > kMaxDim || c > kMaxDim || std::min(m, c) > kMaxShort || m * c > kMaxElems)
+    // The Newton-Schulz buffers are addressed with 32-bit byte offsets: the
+    // canonical matrix padded to multiples of 256 must stay below 2^31 elements.
+    if (m > kMaxDim || c > kMaxDim || std::min(m, c) > kMaxShort || m * c > kMaxElems ||
+        pad_to(m, 256) * pad_to(c, 256) > kMaxElems)
       return fail(MALT_ERR_SHAPE, "matrix %d: %lld x %lld exceeds the supported size "
-                  "(dims <= 2^20, min dim <= 32768, elements < 2^31)", i, (long long)m, (long long)c);
+                  "(dims <= 2^20, min dim <= 32768, elements (padded to multiples of 256) < 2^31)", i,
+                  (long long)m, (long long)c);
   }
   return MALT_OK;
 }

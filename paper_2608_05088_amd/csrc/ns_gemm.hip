@@ -101,15 +101,32 @@ __device__ __forceinline__ void wait_vm_c() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-// One 16-byte-per-lane direct load into LDS at the wave-uniform address
-// lds_addr (lane i writes lds_addr + 16 i).  Issued from inline assembly so the
-// compiler does not track it: it cannot tell the ring slot being filled from
-// the slot being read, and before the transposed reads of the update it would
-// wait for each stage's loads right after issuing them.  Completion is ordered
-// by the pipeline's explicit vmcnt waits and barriers; m0 carries the LDS
-// address and needs one wait state after its write.
-__device__ __forceinline__ void dma16(const void* g, uint32_t lds_addr) {
-  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(g), "{m0}"(lds_addr) : "memory");
+// Operands are read through buffer resources (base address in scalar
+// registers, unbounded range, raw addressing): the buffer form of the direct
+// load moves more bytes per clock into LDS than the flat-address form.
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ i32x4 buf_rsrc(const void* base) {
+  const uint64_t b = (uint64_t)(uintptr_t)base;
+  i32x4 r;
+  r.x = (int)(uint32_t)b;
+  r.y = (int)(uint32_t)((b >> 32) & 0xFFFFu);   // stride 0
+  r.z = -1;                                      // num_records: no clamping below 4 GB
+  r.w = 0x00020000;                              // 32-bit data format, raw access
+  return r;
+}
+
+// One 16-byte-per-lane direct load into LDS: lane i reads base + soff + voff_i
+// and writes lds_addr + 16 i (lds_addr wave-uniform).  Issued from inline
+// assembly so the compiler does not track it: it cannot tell the ring slot
+// being filled from the slot being read, and before the transposed reads of
+// the update it would wait for each stage's loads right after issuing them.
+// Completion is ordered by the pipeline's explicit vmcnt waits and barriers;
+// m0 carries the LDS address and needs one wait state after its write.
+__device__ __forceinline__ void dma16(const i32x4& rsrc, uint32_t voff, uint32_t soff, uint32_t lds_addr) {
+  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
+               :
+               : "v"(voff), "s"(rsrc), "s"(soff), "{m0}"(lds_addr)
+               : "memory");
 }
 
 // LDS byte address of a generic pointer into LDS: its low 32 bits (the flat
@@ -137,13 +154,15 @@ __device__ __forceinline__ int swz_kn(int k, int n) {
 // At the barrier inside iteration kt, stages up to kt + STAGES - 1 have been
 // issued and stage kt + 1 is awaited; after it, slot kt % STAGES (already
 // read by every wave) receives stage kt + STAGES.
+// nl is the number of loads this wave issues per stage (at most LOADS).
 template <class Issue, class Read, class Mma>
-__device__ __forceinline__ void pipeline(const int KT, char* lds, Issue&& issue, Read&& read, Mma&& mma) {
+__device__ __forceinline__ void pipeline(const int KT, const int nl, char* lds, Issue&& issue, Read&& read,
+                                         Mma&& mma) {
   auto ahead = [&](int j) { return min(STAGES - 2, KT - 1 - j); };
 #pragma unroll
   for (int s = 0; s < STAGES; ++s)
     if (s < KT) issue(s);
-  wait_vm(min(STAGES - 1, KT - 1) * LOADS);
+  wait_vm(min(STAGES - 1, KT - 1) * nl);
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
   read(0, lds, 0);
@@ -157,8 +176,12 @@ __device__ __forceinline__ void pipeline(const int KT, char* lds, Issue&& issue,
         read(c ^ 1, st, h + 1);
       } else if (steady || kt + 1 < KT) {
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // this wave's reads of stage kt are done
-        if constexpr (steady) wait_vm_c<(STAGES - 2) * LOADS>();
-        else wait_vm(ahead(kt + 1) * LOADS);
+        if constexpr (steady) {
+          if constexpr (STAGES == 2) wait_vm_c<0>();
+          else wait_vm((STAGES - 2) * nl);
+        } else {
+          wait_vm(ahead(kt + 1) * nl);
+        }
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
         if constexpr (steady) issue(kt + STAGES);
@@ -196,13 +219,18 @@ void ns_gemm_sym_kernel(NsArgs args) {
   const int ld = (phase == PH_GRAM) ? np : mp;
   const int K = ld;
   const int row0 = t.ti * NS_TILE, col0 = t.tj * NS_TILE;
+  // A diagonal tile's row and column panels are the same rows of P: it loads
+  // the row panel only and reads both operands from it.
+  const bool diag = t.ti == t.tj;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wr = wave / 4, wc = wave % 4;
 
   // Direct-load sources: instruction g < LOADS_PER_OPER covers rows of the
-  // tile-row panel, the rest rows of the tile-column panel (both of P).
-  const bf16_t* src[LOADS];
+  // tile-row panel, the rest rows of the tile-column panel (both of P); byte
+  // offsets into P's buffer (the padded canonical matrix is below 4 GB).
+  const i32x4 rsP = buf_rsrc(P);
+  uint32_t voff[LOADS];
   int dst_off[LOADS];
 #pragma unroll
   for (int q = 0; q < LOADS; ++q) {
@@ -210,7 +238,7 @@ void ns_gemm_sym_kernel(NsArgs args) {
     const int op = g / LOADS_PER_OPER, qi = g % LOADS_PER_OPER;
     const int row = qi * ROWS_PER_LOAD + lane / CPR;
     const int kc = (lane % CPR) ^ ((row / RPP) % CPR);
-    src[q] = P + (size_t)((op ? col0 : row0) + row) * ld + kc * 8;
+    voff[q] = (uint32_t)(((size_t)((op ? col0 : row0) + row) * ld + kc * 8) * 2);
     dst_off[q] = op * OPER_BYTES + qi * 1024;
   }
   int offa[I][H], offb[J][H];
@@ -220,7 +248,7 @@ void ns_gemm_sym_kernel(NsArgs args) {
 #pragma unroll
     for (int i = 0; i < I; ++i) offa[i][h] = swz_rk(wr * TM + i * 32 + (lane & 31), kc);
 #pragma unroll
-    for (int j = 0; j < J; ++j) offb[j][h] = OPER_BYTES + swz_rk(wc * TN + j * 32 + (lane & 31), kc);
+    for (int j = 0; j < J; ++j) offb[j][h] = (diag ? 0 : OPER_BYTES) + swz_rk(wc * TN + j * 32 + (lane & 31), kc);
   }
 
   f32x16 acc[I][J];
@@ -232,14 +260,16 @@ void ns_gemm_sym_kernel(NsArgs args) {
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
   bf16x8 fa[2][I], fb[2][J];
 
+  // With 8 waves, g = wave + 8q < LOADS_PER_OPER exactly for q < LOADS / 2:
+  // the first half of a wave's loads are row-panel loads.
+  static_assert(LOADS_PER_OPER == (LOADS / 2) * NW, "row-panel loads are the first half");
   pipeline(
-      K / BK, lds,
+      K / BK, diag ? LOADS / 2 : LOADS, lds,
       [&](int kt) {
         char* base = lds + (kt % STAGES) * STAGE_BYTES;
 #pragma unroll
         for (int q = 0; q < LOADS; ++q)
-          __builtin_amdgcn_global_load_lds((const gbl_void_t*)(src[q] + kt * BK), (lds_void_t*)(base + dst_off[q]),
-                                           16, 0, 0);
+          if (q < LOADS / 2 || !diag) dma16(rsP, voff[q], (uint32_t)(kt * BK * 2), lds_u32(base + dst_off[q]));
       },
       [&](int buf, const char* st, int h) {
 #pragma unroll
@@ -387,25 +417,29 @@ void ns_update_kernel(NsArgs args) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wr = wave / 4, wc = wave % 4;
 
-  const bf16_t* src[LOADS];
+  // Direct-load sources as byte offsets into the B' and X buffers: load
+  // g < LOADS_P covers B' rows, the rest X k-rows of the tile.
+  const i32x4 rsB = buf_rsrc(Bm);
+  const i32x4 rsX = buf_rsrc(X);
+  // With 8 waves, g = wave + 8q < LOADS_P exactly for q < LOADS / 2, so which
+  // operand a load reads is known at compile time.
+  static_assert(LOADS_P == (LOADS / 2) * NW, "B' loads are the first half");
+  uint32_t voff[LOADS];
   int dst_off[LOADS];
-  bool isx[LOADS];
 #pragma unroll
   for (int q = 0; q < LOADS; ++q) {
     const int g = wave + q * NW;
-    if (g < LOADS_P) {
+    if (q < LOADS / 2) {
       const int row = g * ROWS_PER_LOAD + lane / CPR;
       const int kc = (lane % CPR) ^ ((row / RPP) % CPR);
-      src[q] = Bm + (size_t)(row0 + row) * ldb + kc * 8;
+      voff[q] = (uint32_t)(((size_t)(row0 + row) * ldb + kc * 8) * 2);
       dst_off[q] = g * 1024;
-      isx[q] = false;
     } else {
       const int qi = g - LOADS_P;
       const int k = qi * KROWS_PER_LOAD + lane / 32;
       const int c = (lane % 32) ^ (4 * (k & 3));   // logical 16-byte chunk of this physical slot
-      src[q] = X + (size_t)k * np + col0 + c * 8;
+      voff[q] = (uint32_t)(((size_t)k * np + col0 + c * 8) * 2);
       dst_off[q] = OPER_BYTES + qi * 1024;
-      isx[q] = true;
     }
   }
   // B' fragments: rows of the output, k contiguous.
@@ -440,14 +474,16 @@ void ns_update_kernel(NsArgs args) {
   bf16x8 fx[2][NA], fb[2][NB];
 
   pipeline(
-      K / BK, lds,
+      K / BK, LOADS, lds,
       [&](int kt) {
         const int k0 = kt * BK;
         const int k0x = k0 >= mp ? k0 - mp : k0;   // X's k wraps for split matrices
         char* base = lds + (kt % STAGES) * STAGE_BYTES;
 #pragma unroll
-        for (int q = 0; q < LOADS; ++q)
-          dma16(isx[q] ? src[q] + (size_t)k0x * np : src[q] + k0, lds_u32(base + dst_off[q]));
+        for (int q = 0; q < LOADS / 2; ++q) dma16(rsB, voff[q], (uint32_t)(k0 * 2), lds_u32(base + dst_off[q]));
+#pragma unroll
+        for (int q = LOADS / 2; q < LOADS; ++q)
+          dma16(rsX, voff[q], (uint32_t)((size_t)k0x * np * 2), lds_u32(base + dst_off[q]));
       },
       [&](int buf, const char* st, int h) {
 #pragma unroll

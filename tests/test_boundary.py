@@ -83,6 +83,7 @@ def test_workspace_scales_with_ns_buffers(L):
     ([(1 << 21, 2)], lm.MALT_ERR_SHAPE),
     ([(40000, 40000)], lm.MALT_ERR_SHAPE),
     ([(65536, 65536)], lm.MALT_ERR_SHAPE),
+    ([(2047, 1 << 20)], lm.MALT_ERR_SHAPE),   # < 2^31 elements, 2^31 once padded to 256
 ])
 def test_state_size_rejects_bad_shapes(L, shapes, code):
     sb, wb = c_size_t(0), c_size_t(0)
