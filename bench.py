@@ -94,12 +94,22 @@ def cpu_baseline(w, layers: int):
         sample_desc.append(f"{s[0]}x{s[1]}")
     total_s = sum(per_shape[s] for s in shapes)
     sampled_s = sum(per_shape[s] * layers for s in uniq)
-    threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+    blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+    threads = max([p.get("num_threads", 1) for p in blas] or [1])
+    cpu_model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu_model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     return {"value": total_s * 1e3, "unit": "ms per step (extrapolated per shape)", "cores": int(threads),
             "kind": "oracle",
             "sample": f"one oracle step on {layers} matrix of each shape ({', '.join(sample_desc)}), "
                       f"{sampled_s:.1f} s of CPU time, scaled by shape counts to all {len(shapes)} matrices",
-            "host_cpus": os.cpu_count()}
+            "host_cpus": os.cpu_count(), "affinity_cpus": len(os.sched_getaffinity(0)), "cpu_model": cpu_model,
+            "blas": ", ".join(f"{p.get('internal_api')} {p.get('version')}" for p in blas)}
 
 
 def main():
@@ -186,11 +196,16 @@ def main():
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": recorded_traffic(w.name),
                 "flops_per_launch": flops_per_launch, "avg_launch_ms": round(avg_launch_s * 1e3, 4),
                 "flops_basis": "2 m'^2 n' per matrix per launch (B'X)"}
+    # Dense-equivalent count (4 m'^2 n' + 2 m'^3 per iteration): the Gram and
+    # polynomial products counted without their symmetry.
+    dense_step = 2 * prof["ns_gram"]["flops"] + 2 * prof["ns_poly"]["flops"] + prof["ns_update"]["flops"]
     ns_all = {"kernels": "ns_gemm_sym_kernel + ns_update_kernel", "ms_per_step": round(ns_ms / K, 4),
               "TFLOP_per_s": round(ns_flops_step * K / (ns_ms * 1e-3) / 1e12, 1),
               "frac": round(ns_flops_step * K / (ns_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
               "flops_per_step": ns_flops_step,
-              "flops_basis": "symmetric minimum 3 m'^2 n' + m'^3 per matrix per NS iteration"}
+              "flops_basis": "symmetric minimum 3 m'^2 n' + m'^3 per matrix per NS iteration",
+              "dense_equiv_TFLOP_per_s": round(dense_step * K / (ns_ms * 1e-3) / 1e12, 1),
+              "dense_equiv_basis": "4 m'^2 n' + 2 m'^3 per matrix per NS iteration"}
     ew_bytes = sum(prof[k]["bytes"] for k in ("momentum_rowcol", "scale_convert", "backmap_write"))
     ew_ms = sum(prof[k]["ms"] for k in ("momentum_rowcol", "scale_convert", "backmap_write")) / K
     hbm = {"elementwise_GB_per_s": round(ew_bytes / (ew_ms * 1e-3) / 1e9, 1),

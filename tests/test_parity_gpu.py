@@ -244,3 +244,20 @@ def test_c4_gpt2_large_sampled():
     o = run_oracle(list(w.shapes), w.variant, W0, grads, _hp(w), collect=sample)
     worst = compare(g, o, w.variant, label="C4")
     say(f"[parity] C4 worst {worst}")
+
+
+@pytest.mark.slow
+def test_c5_stress_subset_two_steps():
+    # C5's two shapes at full size (4096 x 4096 and 4096 x 11008, Student-t
+    # gradients), two MALTER steps so alpha departs from 1.  The plan holds the
+    # subset only: the step is independent per matrix.
+    w = wl.WORKLOADS[5]
+    idx = [0, 1]
+    shapes = [w.shapes[i] for i in idx]
+    say(f"[parity] C5 subset {shapes} {w.variant} x2")
+    W0, grads = _inputs(w, 2, indices=idx)
+    g = run_gpu(shapes, w.variant, W0, grads, _hp(w))
+    o = run_oracle(shapes, w.variant, W0, grads, _hp(w))
+    worst = compare(g, o, w.variant, label="C5")
+    assert abs(g[1].scal[1]["alpha"] - 1.0) > 1e-3
+    say(f"[parity] C5 worst {worst}")
