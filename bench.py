@@ -38,6 +38,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="gpt2_large")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-vendor-ref", action="store_true",
+                    help="skip timing torch.bmm (hipBLASLt) on the update products")
     ap.add_argument("--cpu-sample-layers", type=int, default=12)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run one plain 1 GiB device-to-device copy (HBM counter calibration)")
@@ -59,6 +61,38 @@ def recorded_traffic(workload: str):
     if fields.get("source_sha256") != sha or "traffic_bytes_per_launch" not in fields:
         return None
     return float(fields["traffic_bytes_per_launch"])
+
+
+def vendor_gemm_reference(w, dev):
+    """Time the vendor bf16 GEMM (hipBLASLt through torch.bmm) on the update
+    product of the workload, B'X for every matrix, one batched call per
+    distinct canonical shape: context for the update kernel's rate."""
+    import torch
+    groups = {}
+    for (r, c) in w.shapes:
+        mp, np_ = min(r, c), max(r, c)
+        groups[(mp, np_)] = groups.get((mp, np_), 0) + 1
+    total_ms, total_flops, per = 0.0, 0.0, {}
+    for (mp, np_), cnt in sorted(groups.items()):
+        B = torch.randn(cnt, mp, mp, device=dev, dtype=torch.bfloat16)
+        X = torch.randn(cnt, mp, np_, device=dev, dtype=torch.bfloat16)
+        for _ in range(3):
+            torch.bmm(B, X)
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        s.record()
+        for _ in range(10):
+            torch.bmm(B, X)
+        e.record()
+        torch.cuda.synchronize()
+        ms = s.elapsed_time(e) / 10
+        flops = 2.0 * cnt * mp * mp * np_
+        per[f"{cnt}x({mp}x{mp} @ {mp}x{np_})"] = round(flops / (ms * 1e-3) / 1e12, 1)
+        total_ms += ms
+        total_flops += flops
+        del B, X
+    return {"what": "torch.bmm bf16 (hipBLASLt) on the same B'X products, one batched call per shape",
+            "TFLOP_per_s": round(total_flops / (total_ms * 1e-3) / 1e12, 1), "per_shape_TFLOP_per_s": per}
 
 
 def cpu_baseline(w, layers: int):
@@ -214,6 +248,9 @@ def main():
     plan.close()
     del grad_sets, Wd
     torch.cuda.empty_cache()
+    vendor = None if args.no_vendor_ref else vendor_gemm_reference(w, dev)
+    if vendor is not None:
+        roofline["vendor_gemm_reference"] = vendor
     if args.copy_calibration:
         # A plain copy kernel of known size (an elementwise x*1 kernel, not the
         # SDMA engine): 2^30 bytes read, 2^30 bytes written.

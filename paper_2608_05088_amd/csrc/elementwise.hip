@@ -121,84 +121,121 @@ __global__ __launch_bounds__(NTHREADS) void precond_finalize_kernel(EwArgs a) {
 // X0 = bf16(L M R) in the canonical orientation (W for wide matrices, W^T
 // through an LDS transpose for tall ones) over the zero-padded domain, plus
 // per-tile sums of (LMR)^2 and, for MALTER, (LGR)^2.  Tiles cover W-oriented
-// padded rows x cols in K2_T x K2_T blocks.
+// padded rows x cols in K2_T x K2_T blocks, K2_GROUP tiles per workgroup.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(NTHREADS) void scale_convert_kernel(EwArgs a) {
-  __shared__ bf16_t tsh[K2_T][K2_T + 2];
-  __shared__ float red[2][4];
-  const Tile t = a.tiles[xcd_remap(blockIdx.x, gridDim.x)];
+  // One workgroup converts K2_GROUP consecutive tiles: a 64-row band of
+  // K2_GROUP * 64 W columns of one matrix (a matrix's tiles are listed band by
+  // band, and every band holds a multiple of K2_GROUP tiles).  All loads of the
+  // band are issued before any conversion.
+  constexpr int TG = K2_GROUP;
+  __shared__ bf16_t tsh[TG][K2_T][K2_T + 2];
+  __shared__ float red[2 * TG][4];
+  const int grp = xcd_remap(blockIdx.x, gridDim.x);
+  const Tile t = a.tiles[grp * TG];
   const MatDesc& d = a.desc[t.mat];
   const int m = d.m, n = d.n;
   const bool vec = a.ptrs[t.mat].vec != 0;
   bf16_t* __restrict__ X0 = d.X[0];
   const int ldx = d.np;                  // canonical row pitch
+  const float* __restrict__ M = d.M;
   const float* __restrict__ G = a.ptrs[t.mat].G;
-  const int r0 = t.ti * K2_T, c0 = t.tj * K2_T;
-  const int cc = (threadIdx.x & 15) * 4;
-  float s2 = 0.f, q2 = 0.f;
-  float Rv[4];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) Rv[e] = (c0 + cc + e < n) ? d.Rv[c0 + cc + e] : 0.f;
+  const bool malter = a.malter != 0;
+  const int r0 = t.ti * K2_T, cb = t.tj * K2_T;   // band columns cb .. cb + TG*K2_T
+  const int cc = (threadIdx.x & 15) * 4;          // 4 columns of each tile
+  const int rq = threadIdx.x >> 4;                // rows rq + 16p, p = 0..3
+
+  float Li[4];
 #pragma unroll
   for (int p = 0; p < 4; ++p) {
-    const int rr = p * 16 + (threadIdx.x >> 4);
-    const int r = r0 + rr;
-    float x[4] = {0.f, 0.f, 0.f, 0.f};
-    if (r < m) {
-      const float Li = d.Lv[r];
-      float mm[4];
-      load4(d.M + (size_t)r * n, c0 + cc, n, vec, mm);
+    const int r = r0 + p * 16 + rq;
+    Li[p] = r < m ? d.Lv[r] : 0.f;
+  }
+  float Rv[TG][4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        x[e] = Li * mm[e] * Rv[e];
-        s2 += x[e] * x[e];
-      }
-      if (a.malter) {
-        float g[4];
-        load4(G + (size_t)r * n, c0 + cc, n, vec, g);
+  for (int j = 0; j < TG; ++j)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float y = Li * g[e] * Rv[e];
-          q2 += y * y;
-        }
+    for (int e = 0; e < 4; ++e) {
+      const int c = cb + j * K2_T + cc + e;
+      Rv[j][e] = c < n ? d.Rv[c] : 0.f;
+    }
+  float mm[TG][4][4], gg[TG][4][4];
+#pragma unroll
+  for (int j = 0; j < TG; ++j)
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int r = r0 + p * 16 + rq;
+      const int c = cb + j * K2_T + cc;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) mm[j][p][e] = gg[j][p][e] = 0.f;
+      if (r < m) {
+        load4(M + (size_t)r * n, c, n, vec, mm[j][p]);
+        if (malter) load4(G + (size_t)r * n, c, n, vec, gg[j][p]);
       }
     }
-    uint2 pk;
-    pk.x = pack_bf16x2(x[0], x[1]);
-    pk.y = pack_bf16x2(x[2], x[3]);
-    if (!d.tall) {
-      *reinterpret_cast<uint2*>(X0 + (size_t)r * ldx + c0 + cc) = pk;
-    } else {
-      tsh[rr][cc + 0] = (bf16_t)(pk.x & 0xffffu);
-      tsh[rr][cc + 1] = (bf16_t)(pk.x >> 16);
-      tsh[rr][cc + 2] = (bf16_t)(pk.y & 0xffffu);
-      tsh[rr][cc + 3] = (bf16_t)(pk.y >> 16);
+
+  float s2[TG], q2[TG];
+#pragma unroll
+  for (int j = 0; j < TG; ++j) {
+    s2[j] = 0.f;
+    q2[j] = 0.f;
+    const int c0 = cb + j * K2_T;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int rr = p * 16 + rq;
+      float x[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        x[e] = Li[p] * mm[j][p][e] * Rv[j][e];
+        s2[j] += x[e] * x[e];
+        const float y = Li[p] * gg[j][p][e] * Rv[j][e];   // zero for MALT (gg = 0)
+        q2[j] += y * y;
+      }
+      uint2 pk;
+      pk.x = pack_bf16x2(x[0], x[1]);
+      pk.y = pack_bf16x2(x[2], x[3]);
+      if (!d.tall) {
+        *reinterpret_cast<uint2*>(X0 + (size_t)(r0 + rr) * ldx + c0 + cc) = pk;
+      } else {
+        tsh[j][rr][cc + 0] = (bf16_t)(pk.x & 0xffffu);
+        tsh[j][rr][cc + 1] = (bf16_t)(pk.x >> 16);
+        tsh[j][rr][cc + 2] = (bf16_t)(pk.y & 0xffffu);
+        tsh[j][rr][cc + 3] = (bf16_t)(pk.y >> 16);
+      }
     }
   }
   if (d.tall) {
     __syncthreads();
-    // Transposed write: thread -> (W column ct, 16-row segment).
+    // Transposed write: thread -> (W column ct, 16-row segment) of each tile.
     const int ct = threadIdx.x >> 2;
     const int seg = (threadIdx.x & 3) * 16;
-    uint32_t wv[8];
 #pragma unroll
-    for (int k = 0; k < 8; ++k)
-      wv[k] = (uint32_t)tsh[seg + 2 * k][ct] | ((uint32_t)tsh[seg + 2 * k + 1][ct] << 16);
-    uint4* dst = reinterpret_cast<uint4*>(X0 + (size_t)(c0 + ct) * ldx + r0 + seg);
-    dst[0] = make_uint4(wv[0], wv[1], wv[2], wv[3]);
-    dst[1] = make_uint4(wv[4], wv[5], wv[6], wv[7]);
+    for (int j = 0; j < TG; ++j) {
+      uint32_t wv[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        wv[k] = (uint32_t)tsh[j][seg + 2 * k][ct] | ((uint32_t)tsh[j][seg + 2 * k + 1][ct] << 16);
+      uint4* dst = reinterpret_cast<uint4*>(X0 + (size_t)(cb + j * K2_T + ct) * ldx + r0 + seg);
+      dst[0] = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+      dst[1] = make_uint4(wv[4], wv[5], wv[6], wv[7]);
+    }
   }
-  s2 = wave_sum(s2);
-  q2 = wave_sum(q2);
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  if (lane == 0) {
-    red[0][w] = s2;
-    red[1][w] = q2;
+#pragma unroll
+  for (int j = 0; j < TG; ++j) {
+    const float sj = wave_sum(s2[j]);
+    const float qj = wave_sum(q2[j]);
+    if (lane == 0) {
+      red[2 * j][w] = sj;
+      red[2 * j + 1][w] = qj;
+    }
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
-    d.k2part[2 * (size_t)t.idx + 0] = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
-    d.k2part[2 * (size_t)t.idx + 1] = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
+  if (threadIdx.x < TG) {
+    const int j = threadIdx.x;
+    d.k2part[2 * (size_t)(t.idx + j) + 0] = (red[2 * j][0] + red[2 * j][1]) + (red[2 * j][2] + red[2 * j][3]);
+    d.k2part[2 * (size_t)(t.idx + j) + 1] =
+        (red[2 * j + 1][0] + red[2 * j + 1][1]) + (red[2 * j + 1][2] + red[2 * j + 1][3]);
   }
 }
 
@@ -332,7 +369,8 @@ hipError_t launch_precond_finalize(const EwArgs& a, hipStream_t s) {
 }
 hipError_t launch_scale_convert(const EwArgs& a, hipStream_t s) {
   if (a.ntiles == 0) return hipSuccess;
-  hipLaunchKernelGGL(scale_convert_kernel, dim3(a.ntiles), dim3(NTHREADS), 0, s, a);
+  if (a.ntiles % K2_GROUP != 0) return hipErrorInvalidValue;   // bands hold whole groups
+  hipLaunchKernelGGL(scale_convert_kernel, dim3(a.ntiles / K2_GROUP), dim3(NTHREADS), 0, s, a);
   return hipGetLastError();
 }
 hipError_t launch_norm_scalars(const EwArgs& a, int32_t nmat, hipStream_t s) {

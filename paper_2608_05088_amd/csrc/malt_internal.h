@@ -10,8 +10,11 @@ namespace malt {
 // 256-thread workgroup; each lane owns 4 consecutive columns.
 constexpr int EW_TR = 32;
 constexpr int EW_TC = 256;
-// Scale+convert tile (with an LDS transpose): K2_T x K2_T.
+// Scale+convert tile (with an LDS transpose): K2_T x K2_T; a workgroup takes
+// K2_GROUP consecutive tiles of one row band (padded W dimensions are
+// multiples of 256 = K2_GROUP * K2_T, so bands hold whole groups).
 constexpr int K2_T = 64;
+constexpr int K2_GROUP = 4;
 // Newton-Schulz output tile and padding unit of the bf16 buffers.
 constexpr int NS_TILE = 256;
 constexpr int NS_BK = 64;
