@@ -43,7 +43,11 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 #ifndef MALT_NS_STAGES
 #define MALT_NS_STAGES 2
 #endif
-constexpr int NW = 8;                                // waves per workgroup
+#ifndef MALT_NS_WAVES
+#define MALT_NS_WAVES 8
+#endif
+constexpr int NW = MALT_NS_WAVES;                    // waves per workgroup (4 or 8)
+constexpr int WPE = NW / 4;                          // waves per SIMD
 constexpr int NT = NW * 64;                          // threads per workgroup
 constexpr int BK = MALT_NS_BK;                       // k per pipeline stage
 constexpr int STAGES = MALT_NS_STAGES;               // LDS ring depth
@@ -64,8 +68,8 @@ static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
 static_assert(H % 2 == 0, "sub-steps per stage must be even");
 static_assert(LOADS * NW * 1024 == 2 * OPER_BYTES, "loads must split evenly over the waves");
 
-// Wave grid 2 x 4: each wave owns TM x TN of the 256 x 256 tile.
-constexpr int TM = NS_TILE / 2, TN = NS_TILE / 4;
+// Wave grid 2 x (NW / 2): each wave owns TM x TN of the 256 x 256 tile.
+constexpr int TM = NS_TILE / 2, TN = NS_TILE / (NW / 2);
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4_t;
@@ -148,25 +152,54 @@ __device__ __forceinline__ int swz_kn(int k, int n) {
 }
 
 // Software pipeline over KT stages shared by both kernels.
-//   issue(kt)        start the direct loads of stage kt into slot kt % STAGES
-//   read(buf, st, h) fragment reads of sub-step h of the stage at st into buf
-//   mma(buf)         the MFMAs of the fragments in buf
-// At the barrier inside iteration kt, stages up to kt + STAGES - 1 have been
-// issued and stage kt + 1 is awaited; after it, slot kt % STAGES (already
-// read by every wave) receives stage kt + STAGES.
-// nl is the number of loads this wave issues per stage (at most LOADS).
+//   issue(kt, i)      the i-th direct load (0 <= i < nl) this wave issues for
+//                     stage kt, into slot kt % STAGES
+//   read(buf, st, h)  fragment reads of sub-step h of the stage at st into buf
+//   mma(buf, after)   the MFMAs of the fragments in buf, calling after(j) once
+//                     the j-th of the NMMA has been issued
+// nl is the number of loads this wave issues per stage (LOADS, or fewer).
+//
+// Burst (two slots): at the barrier closing stage kt, stage kt + 1 has landed
+// and every wave is done with slot kt % 2, which then receives all of stage
+// kt + 2's loads.
+// Spread (three or more slots): stage kt + STAGES - 1 is loaded while stage kt
+// computes, its nl loads spread over the H sub-steps (nl / H per sub-step, each
+// after an equal share of the MFMAs), into the slot stage kt - 1 freed.  The
+// loads of STAGES - 2 stages stay in flight across every barrier, and no wave
+// issues a burst of loads while its SIMD partner waits for the matrix core.
+constexpr int NMMA = (TM / 32) * (TN / 32);   // MFMAs per wave per sub-step
+#ifndef MALT_NS_SPREAD
+#define MALT_NS_SPREAD (MALT_NS_STAGES >= 3)
+#endif
+constexpr bool SPREAD = MALT_NS_SPREAD != 0;
+static_assert(!SPREAD || STAGES >= 3, "spread loads need two stages of lead");
+
 template <class Issue, class Read, class Mma>
 __device__ __forceinline__ void pipeline(const int KT, const int nl, char* lds, Issue&& issue, Read&& read,
                                          Mma&& mma) {
-  auto ahead = [&](int j) { return min(STAGES - 2, KT - 1 - j); };
+  constexpr int PRE = SPREAD ? STAGES - 1 : STAGES;   // stages loaded before the loop
+  // Load indices stay compile-time constants (the kernels index register
+  // arrays with them); a wave issuing nl < LOADS loads skips indices >= nl.
 #pragma unroll
-  for (int s = 0; s < STAGES; ++s)
-    if (s < KT) issue(s);
-  wait_vm(min(STAGES - 1, KT - 1) * nl);
+  for (int s = 0; s < PRE; ++s)
+    if (s < KT)
+#pragma unroll
+      for (int i = 0; i < LOADS; ++i)
+        if (i < nl) issue(s, i);
+  wait_vm(min(PRE - 1, KT - 1) * nl);   // stage 0 has landed
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
   read(0, lds, 0);
+  // Spread: load i of a stage goes out in sub-step i / PER, after MFMA
+  // (i % PER + 1) * GAP - 1; before the last sub-step min(nl, (H-1) PER) of a
+  // stage's loads have been issued.
+  constexpr int PER = LOADS / H;
+  constexpr int GAP = NMMA / PER;
+  static_assert(!SPREAD || (LOADS % H == 0 && NMMA % PER == 0), "loads must spread evenly over the MFMAs");
+  const int early = min(nl, (H - 1) * PER);
   auto body = [&](const int kt, auto steady_tag) {
+    // steady: the stage this iteration loads (burst: kt + 2 at the barrier;
+    // spread: kt + STAGES - 1 over the sub-steps) exists.
     constexpr bool steady = decltype(steady_tag)::value;
     const char* st = lds + (kt % STAGES) * STAGE_BYTES;
 #pragma unroll
@@ -176,29 +209,49 @@ __device__ __forceinline__ void pipeline(const int KT, const int nl, char* lds, 
         read(c ^ 1, st, h + 1);
       } else if (steady || kt + 1 < KT) {
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // this wave's reads of stage kt are done
-        if constexpr (steady) {
-          if constexpr (STAGES == 2) wait_vm_c<0>();
-          else wait_vm((STAGES - 2) * nl);
+        if constexpr (SPREAD) {
+          // In flight after stage kt + 1: whole stages kt + 2 .. kt + STAGES - 2
+          // and, when it exists, all but the last sub-step's share of stage
+          // kt + STAGES - 1.
+          if constexpr (steady) wait_vm((STAGES - 3) * nl + early);
+          else wait_vm(max(0, min(kt + STAGES - 2, KT - 1) - (kt + 1)) * nl);
         } else {
-          wait_vm(ahead(kt + 1) * nl);
+          if constexpr (steady) {
+            if constexpr (STAGES == 2) wait_vm_c<0>();
+            else wait_vm((STAGES - 2) * nl);
+          } else {
+            wait_vm(min(STAGES - 2, KT - 1 - (kt + 1)) * nl);
+          }
         }
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
-        if constexpr (steady) issue(kt + STAGES);
+        if constexpr (!SPREAD && steady) {
+#pragma unroll
+          for (int i = 0; i < LOADS; ++i)
+            if (i < nl) issue(kt + STAGES, i);
+        }
         read(c ^ 1, lds + ((kt + 1) % STAGES) * STAGE_BYTES, 0);
       }
-      mma(c);
+      mma(c, [&](int j) {
+        if constexpr (SPREAD && steady) {
+          if ((j + 1) % GAP == 0) {
+            const int i = h * PER + j / GAP;
+            if (i < nl) issue(kt + STAGES - 1, i);
+          }
+        }
+      });
     }
   };
+  constexpr int LEAD = SPREAD ? STAGES - 1 : STAGES;
   int kt = 0;
-  for (; kt < KT - STAGES; ++kt) body(kt, std::true_type{});
+  for (; kt < KT - LEAD; ++kt) body(kt, std::true_type{});
   for (; kt < KT; ++kt) body(kt, std::false_type{});
 }
 
 // ===========================================================================
 // Gram and polynomial phases: C = P Q^T, symmetric output, upper tiles.
 // ===========================================================================
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
 void ns_gemm_sym_kernel(NsArgs args) {
   constexpr int I = TM / 32, J = TN / 32;    // 32x32 blocks per wave
   constexpr int ROWS_PER_LOAD = 1024 / RB;
@@ -224,7 +277,7 @@ void ns_gemm_sym_kernel(NsArgs args) {
   const bool diag = t.ti == t.tj;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wr = wave / 4, wc = wave % 4;
+  const int wr = wave / (NW / 2), wc = wave % (NW / 2);
 
   // Direct-load sources: instruction g < LOADS_PER_OPER covers rows of the
   // tile-row panel, the rest rows of the tile-column panel (both of P); byte
@@ -265,11 +318,8 @@ void ns_gemm_sym_kernel(NsArgs args) {
   static_assert(LOADS_PER_OPER == (LOADS / 2) * NW, "row-panel loads are the first half");
   pipeline(
       K / BK, diag ? LOADS / 2 : LOADS, lds,
-      [&](int kt) {
-        char* base = lds + (kt % STAGES) * STAGE_BYTES;
-#pragma unroll
-        for (int q = 0; q < LOADS; ++q)
-          if (q < LOADS / 2 || !diag) dma16(rsP, voff[q], (uint32_t)(kt * BK * 2), lds_u32(base + dst_off[q]));
+      [&](int kt, int i) {   // diagonal tiles issue the row-panel loads q < LOADS / 2 only
+        dma16(rsP, voff[i], (uint32_t)(kt * BK * 2), lds_u32(lds + (kt % STAGES) * STAGE_BYTES + dst_off[i]));
       },
       [&](int buf, const char* st, int h) {
 #pragma unroll
@@ -277,12 +327,14 @@ void ns_gemm_sym_kernel(NsArgs args) {
 #pragma unroll
         for (int j = 0; j < J; ++j) fb[buf][j] = *reinterpret_cast<const bf16x8*>(st + offb[j][h]);
       },
-      [&](int buf) {
+      [&](int buf, auto&& after) {
 #pragma unroll
         for (int i = 0; i < I; ++i)
 #pragma unroll
-          for (int j = 0; j < J; ++j)
+          for (int j = 0; j < J; ++j) {
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[buf][i], fb[buf][j], acc[i][j], 0, 0, 0);
+            after(i * J + j);
+          }
       });
 
   // ---------------------------------------------------------------- epilogue
@@ -387,7 +439,7 @@ void ns_gemm_sym_kernel(NsArgs args) {
 // ===========================================================================
 // Update phase: X' = s B' X  (NN), computed as C^T = X^T B'^T blocks.
 // ===========================================================================
-__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
 void ns_update_kernel(NsArgs args) {
   constexpr int NB = TM / 32;                // B' fragments (output rows, MFMA B operand)
   constexpr int NA = TN / 32;                // X fragments (output cols, MFMA A operand)
@@ -415,7 +467,7 @@ void ns_update_kernel(NsArgs args) {
   const int row0 = t.ti * NS_TILE, col0 = t.tj * NS_TILE;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wr = wave / 4, wc = wave % 4;
+  const int wr = wave / (NW / 2), wc = wave % (NW / 2);
 
   // Direct-load sources as byte offsets into the B' and X buffers: load
   // g < LOADS_P covers B' rows, the rest X k-rows of the tile.
@@ -475,15 +527,12 @@ void ns_update_kernel(NsArgs args) {
 
   pipeline(
       K / BK, LOADS, lds,
-      [&](int kt) {
+      [&](int kt, int q) {   // q < LOADS / 2: B' rows, else X k-rows
         const int k0 = kt * BK;
         const int k0x = k0 >= mp ? k0 - mp : k0;   // X's k wraps for split matrices
-        char* base = lds + (kt % STAGES) * STAGE_BYTES;
-#pragma unroll
-        for (int q = 0; q < LOADS / 2; ++q) dma16(rsB, voff[q], (uint32_t)(k0 * 2), lds_u32(base + dst_off[q]));
-#pragma unroll
-        for (int q = LOADS / 2; q < LOADS; ++q)
-          dma16(rsX, voff[q], (uint32_t)((size_t)k0x * np * 2), lds_u32(base + dst_off[q]));
+        const uint32_t la = lds_u32(lds + (kt % STAGES) * STAGE_BYTES + dst_off[q]);
+        if (q < LOADS / 2) dma16(rsB, voff[q], (uint32_t)(k0 * 2), la);
+        else dma16(rsX, voff[q], (uint32_t)((size_t)k0x * np * 2), la);
       },
       [&](int buf, const char* st, int h) {
 #pragma unroll
@@ -497,12 +546,14 @@ void ns_update_kernel(NsArgs args) {
           fx[buf][a] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
         }
       },
-      [&](int buf) {
+      [&](int buf, auto&& after) {
 #pragma unroll
         for (int a = 0; a < NA; ++a)
 #pragma unroll
-          for (int b = 0; b < NB; ++b)
+          for (int b = 0; b < NB; ++b) {
             acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fx[buf][a], fb[buf][b], acc[a][b], 0, 0, 0);
+            after(a * NB + b);
+          }
       });
 
   // ---------------------------------------------------------------- epilogue
