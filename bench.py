@@ -11,7 +11,7 @@ HBM bandwidth / throughput, and the fp64 CPU oracle timed on a bounded sample
 of the same workload (cpu_baseline).
 
   python bench.py [--steps K] [--warmup W] [--workload gpt2_large|gpt2_small|gpt2_medium|single_256x512|stress_4096]
-                  [--no-cpu-baseline] [--gpus 1]
+                  [--no-cpu-baseline] [--no-vendor-ref] [--small-case] [--gpus 1]
 """
 from __future__ import annotations
 
@@ -38,6 +38,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="gpt2_large")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--small-case", action="store_true",
+                    help="also report the step latency of the single 256 x 512 matrix workload "
+                         "(off by default so kernel traces of the default run cover one workload)")
     ap.add_argument("--no-vendor-ref", action="store_true",
                     help="skip timing torch.bmm (hipBLASLt) on the update products")
     ap.add_argument("--cpu-sample-layers", type=int, default=12)
@@ -61,6 +64,35 @@ def recorded_traffic(workload: str):
     if fields.get("source_sha256") != sha or "traffic_bytes_per_launch" not in fields:
         return None
     return float(fields["traffic_bytes_per_launch"])
+
+
+def small_case_latency(lm, wl, dev, reps: int = 50):
+    """Latency of one step on the single 256 x 512 matrix workload (MALT),
+    which is bound by launch latency, not by bandwidth or matrix-core rate:
+    median over `reps` individually timed steps."""
+    import statistics
+
+    import torch
+    w = wl.WORKLOADS[1]
+    shapes = list(w.shapes)
+    Wd = [wl.weight_device(w.cid, i, s, dev) for i, s in enumerate(shapes)]
+    Gd = [wl.grad_device(w.cid, 1, i, s, w.dist, dev) for i, s in enumerate(shapes)]
+    plan = lm.Plan(shapes, w.variant, device=dev)
+    hp = lm.make_hparams(lr=w.lr, mu1=w.mu1, mu2=w.mu2, eps=w.eps)
+    stream = torch.cuda.current_stream()
+    for _ in range(5):
+        plan.step(Wd, Gd, hp, stream=stream)
+    times = []
+    for _ in range(reps):
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record(stream)
+        plan.step(Wd, Gd, hp, stream=stream)
+        e.record(stream)
+        e.synchronize()
+        times.append(s.elapsed_time(e))
+    plan.close()
+    return {"workload": w.name, "median_ms": round(statistics.median(times), 4), "reps": reps,
+            "launches_per_step": 4 + 3 * 5 + 2}
 
 
 def vendor_gemm_reference(w, dev):
@@ -248,6 +280,7 @@ def main():
     plan.close()
     del grad_sets, Wd
     torch.cuda.empty_cache()
+    small = small_case_latency(lm, wl, dev) if args.small_case else None
     vendor = None if args.no_vendor_ref else vendor_gemm_reference(w, dev)
     if vendor is not None:
         roofline["vendor_gemm_reference"] = vendor
@@ -271,6 +304,7 @@ def main():
             "config": {"workload": w.name, "variant": w.variant, "matrices": len(shapes), "params": w.numel,
                        "lr": w.lr, "grad_dist": w.dist, "timed": f"{K} consecutive steps, persistent state"},
             "roofline": roofline, "newton_schulz": ns_all, "hbm": hbm, "kernels": kernels,
+            "small_case_latency": small,
             "cpu_baseline": cpu}
     print(json.dumps(line), flush=True)
 
