@@ -464,3 +464,25 @@ def test_p12_vector_shapes_step():
         Mt = inter[0].M_tilde
         np.testing.assert_allclose(O, _phi(np.linalg.norm(Mt) / (np.linalg.norm(Mt) + NS_EPS))
                                    * Mt / np.linalg.norm(Mt), rtol=1e-12)
+
+
+# P13: a scaled partial permutation keeps every stage entrywise, so the whole
+# step is a closed form (tests/closed_forms.py, written from the update rule):
+# the oracle must reproduce it, zero entries included.
+@pytest.mark.parametrize("shape,k,variant", [((60, 90), 50, "malt"), ((90, 40), 40, "malter"), ((64, 64), 64, "malt")])
+def test_p13_permutation_closed_form(shape, k, variant):
+    from closed_forms import permutation_step, random_permutation_pattern
+    m, n = shape
+    rows, cols, g = random_permutation_pattern(m, n, k, seed=13)
+    G = np.zeros((m, n), np.float32)
+    G[rows, cols] = g.astype(np.float32)
+    gg = G[rows, cols].astype(np.float64)
+    st = oracle_init([shape], variant)
+    hp = OracleHparams(variant=variant, lr=1e-3)
+    W, inter = oracle_step([np.zeros((m, n))], [G], st, hp)
+    l, r, Lv, Rv, dw = permutation_step(m, n, rows, cols, gg, variant, lr=1e-3)
+    assert rel_fro(st.l[0], l) < 1e-12 and rel_fro(st.r[0], r) < 1e-12
+    assert rel_fro(inter[0].Lv, Lv) < 1e-12 and rel_fro(inter[0].Rv, Rv) < 1e-12
+    expect = np.zeros((m, n))
+    expect[rows, cols] = dw
+    assert rel_fro(W[0], expect) < 1e-9

@@ -261,3 +261,73 @@ def test_c5_stress_subset_two_steps():
     worst = compare(g, o, w.variant, label="C5")
     assert abs(g[1].scal[1]["alpha"] - 1.0) > 1e-3
     say(f"[parity] C5 worst {worst}")
+
+
+# Extreme aspect ratios: the split (m' <= 128) contraction with the longest
+# allowed dimension, and a thin tall matrix.
+EXTREME = [(1, 1 << 20), (1 << 20, 2), (3, 700000)]
+
+
+def test_extreme_aspect_ratios():
+    say(f"[parity] extreme aspect ratios {EXTREME} malter x2")
+    W0 = [wl.weight(97, i, s) for i, s in enumerate(EXTREME)]
+    grads = [[wl.grad(97, t, i, s, "row_loguniform") for i, s in enumerate(EXTREME)] for t in (1, 2)]
+    hp = dict(lr=1e-2)
+    g = run_gpu(EXTREME, "malter", W0, grads, hp)
+    o = run_oracle(EXTREME, "malter", W0, grads, hp)
+    worst = compare(g, o, "malter", label="extreme")
+    say(f"[parity] extreme worst {worst}")
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("shape,k,variant", [((300, 500), 300, "malter"), ((32768, 32768), 32768, "malt"),
+                                             ((1 << 20, 1792), 1792, "malter")])
+def test_permutation_closed_form_up_to_max_size(shape, k, variant):
+    # A scaled partial permutation keeps every stage entrywise (closed form in
+    # tests/closed_forms.py, pinned to the oracle on the CPU), and bf16 holds
+    # its pattern exactly: off-pattern entries must come out exactly zero.
+    # Covers the largest accepted shapes: min dimension 32768, and the longest
+    # dimension 2^20 with the padded matrix near 2^31 elements (tall path).
+    import torch
+    from closed_forms import permutation_step, random_permutation_pattern
+    m, n = shape
+    say(f"[parity] permutation closed form {shape} k={k} {variant}")
+    rows, cols, g = random_permutation_pattern(m, n, k, seed=99)
+    g32 = g.astype(np.float32)
+    hp = dict(lr=1e-3, mu1=0.95, mu2=0.99, eps=1e-8)
+    dev = torch.device("cuda:0")
+    rt, ct = torch.from_numpy(rows).to(dev), torch.from_numpy(cols).to(dev)
+    G = torch.zeros(m, n, device=dev)
+    G[rt, ct] = torch.from_numpy(g32).to(dev)
+    W = torch.zeros(m, n, device=dev)
+    plan = lm.Plan([shape], variant)
+    plan.step([W], [G], lm.make_hparams(**hp))
+    torch.cuda.synchronize()
+    l, r, Lv, Rv, dw = permutation_step(m, n, rows, cols, g32.astype(np.float64), variant, **hp)
+    Mg, lg, rg, _ = plan.state_views(0)
+    dvw = plan.debug_views(0)
+    assert rel_fro(lg.double().cpu().numpy(), l) <= TOL_STATE
+    assert rel_fro(rg.double().cpu().numpy(), r) <= TOL_STATE
+    assert rel_fro(dvw["Lv"].double().cpu().numpy(), Lv) <= TOL_STATE
+    assert rel_fro(dvw["Rv"].double().cpu().numpy(), Rv) <= TOL_STATE
+    assert rel_fro(Mg[rt, ct].double().cpu().numpy(), 0.05 * g32.astype(np.float64)) <= TOL_STATE
+    err = rel_fro(W[rt, ct].double().cpu().numpy(), dw)
+    # Off the pattern (W started at zero, so W = dW): exactly zero.
+    rng = np.random.default_rng(7)
+    ri = torch.from_numpy(rng.integers(0, m, 50000)).to(dev)
+    ci = torch.from_numpy(rng.integers(0, n, 50000)).to(dev)
+    on = torch.zeros(m, dtype=torch.int64, device=dev) - 1
+    on[rt] = ct
+    off = on[ri] != ci
+    assert int(off.sum().item()) > 0
+    assert float(W[ri[off], ci[off]].abs().max().item()) == 0.0
+    say(f"[parity] permutation {shape}: dW rel err on the pattern {err:.3e}")
+    assert err <= TOL_NS
+    if m * n <= 1 << 20:   # small case: the oracle itself agrees
+        G0 = np.zeros((m, n), np.float32)
+        G0[rows, cols] = g32
+        o = run_oracle([shape], variant, [np.zeros((m, n), np.float32)], [[G0]], hp)
+        assert rel_fro(W.double().cpu().numpy(), o[0]["inter"][0].dW) <= TOL_NS
+    plan.close()
+    del W, G
+    torch.cuda.empty_cache()
