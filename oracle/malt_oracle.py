@@ -37,7 +37,9 @@ Readings taken where the paper is silent or inconsistent (all configurable):
   * No Nesterov momentum; M_t itself is preconditioned and orthogonalised.
   * Decoupled weight decay (listed in the hyper-parameter table but absent
     from both algorithms) is optional: W <- (1 - eta*lambda) W before the
-    update; lambda = 0 by default.  Parity unpinned for lambda != 0.
+    update (the decoupled rule of AdamW, which the paper cites); lambda = 0
+    by default.  Pinned to torch's AdamW on zero gradients and by its
+    separation from the update (P14).
 """
 from __future__ import annotations
 

@@ -9,7 +9,8 @@ libmalt (MALT / MALTER / Muon), the rest to AdamW; "adamw" trains everything
 with torch's AdamW.  The model trains in float32 (no autocast).  One
 iteration is the paper's global batch: 480 sequences of 1024 tokens
 (Sec. 5.1), here as 60 accumulated micro-batches of 8, then one optimizer
-step; weight decay 0.1 on both parts (hyper-parameter table).
+step; weight decay 0.1 on both parts (hyper-parameter table) and a linear
+warm-up over the first 10% of the run (Sec. 5.1).
 
   python -m paper_2608_05088_amd.train --model gpt2-medium --optim adamw,muon,malt,malter
 
@@ -47,6 +48,9 @@ def build_model(name: str, device, seed: int = 0, n_positions: int = 1024):
 def block_matrix(name: str, p) -> bool:
     """The paper's matrix parameters: attention and MLP weights of each block."""
     return p.dim() == 2 and ".h." in name and name.endswith("weight")
+
+
+from .schedules import lambda_lr, linear_warmup  # noqa: E402
 
 
 def make_optimizer(kind: str, model, lr: float, adamw_lr: float, weight_decay: float = 0.1):
@@ -99,6 +103,8 @@ def run(kind: str, args, device) -> dict:
     torch.cuda.reset_peak_memory_stats(device)
     model = build_model(args.model, device, seed=args.seed)
     opt = make_optimizer(kind, model, args.lr, args.adamw_lr, args.weight_decay)
+    # The paper's protocol: linear warm-up over the first 10% of the run.
+    sched = lambda_lr(opt, linear_warmup(args.warmup + args.iters))
     gen = torch.Generator(device=device)
     gen.manual_seed(args.seed)
     B, T = args.micro_batch, args.seq
@@ -113,6 +119,7 @@ def run(kind: str, args, device) -> dict:
         opt.step()
         e.record()
         opt.zero_grad(set_to_none=True)
+        sched.step()
         return s, e, loss
 
     for _ in range(args.warmup):

@@ -36,27 +36,32 @@ def _split(model):
     return names, (lambda p: id(p) in ids)
 
 
-def _hp_kw(variant, lr):
-    return dict(lr=lr, precond_identity=1) if variant == "muon" else dict(lr=lr)
+def _hp_kw(variant, lr, wd=0.0):
+    kw = dict(lr=lr, weight_decay=wd)
+    if variant == "muon":
+        kw["precond_identity"] = 1
+    return kw
 
 
-@pytest.mark.parametrize("variant", ["malt", "malter", "muon"])
-def test_adapter_matches_oracle_and_adamw(variant):
+@pytest.mark.parametrize("variant,wd", [("malt", 0.0), ("malter", 0.0), ("muon", 0.0), ("malt", 0.1),
+                                        ("malter", 0.1)])
+def test_adapter_matches_oracle_and_adamw(variant, wd):
     """GPT-2 parameter set (2 blocks, d = 256) through the adapter with seeded
     synthetic matrix gradients: every matrix state and update against the
     oracle, every other parameter bitwise against torch's AdamW."""
     import torch
     from paper_2608_05088_amd import workloads as wl
     from paper_2608_05088_amd.optim import MALT
-    say(f"[optim] GPT-2 parameter set, {variant} + AdamW, 3 steps, synthetic gradients")
+    say(f"[optim] GPT-2 parameter set, {variant} + AdamW, weight decay {wd}, 3 steps, synthetic gradients")
     model = _tiny_gpt2()
     ref = copy.deepcopy(model)
     names, filt = _split(model)
     params = dict(model.named_parameters())
     lr, alr = 2e-3, 1e-3
-    opt = MALT(model.parameters(), lr=lr, variant=variant, adamw_lr=alr, matrix_filter=filt)
+    opt = MALT(model.parameters(), lr=lr, variant=variant, adamw_lr=alr, weight_decay=wd, adamw_weight_decay=wd,
+               matrix_filter=filt)
     ref_rest = [p for n, p in ref.named_parameters() if n not in names]
-    ref_opt = torch.optim.AdamW(ref_rest, lr=alr, betas=(0.9, 0.95), eps=1e-8, weight_decay=0.0)
+    ref_opt = torch.optim.AdamW(ref_rest, lr=alr, betas=(0.9, 0.95), eps=1e-8, weight_decay=wd)
     gen = torch.Generator(device="cuda").manual_seed(1)
     W0 = [params[n].detach().cpu().numpy().copy() for n in names]
     shapes = [w.shape for w in W0]
@@ -74,7 +79,7 @@ def test_adapter_matches_oracle_and_adamw(variant):
         opt.zero_grad()
         ref_opt.zero_grad()
         dW.append([params[n].detach().double().cpu().numpy() - b for n, b in zip(names, before)])
-    o = run_oracle(shapes, "malter" if variant == "malter" else "malt", W0, grads, _hp_kw(variant, lr))
+    o = run_oracle(shapes, "malter" if variant == "malter" else "malt", W0, grads, _hp_kw(variant, lr, wd))
     plan = opt.matrix_plan()
     worst = 0.0
     for t in range(3):

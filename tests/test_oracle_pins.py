@@ -486,3 +486,53 @@ def test_p13_permutation_closed_form(shape, k, variant):
     expect = np.zeros((m, n))
     expect[rows, cols] = dw
     assert rel_fro(W[0], expect) < 1e-9
+
+
+# --------------------------------------------------------------------------
+# P14: decoupled weight decay.  The algorithms omit it; the hyper-parameter
+# table sets 0.1 and the paper cites decoupled weight decay (AdamW).  The
+# oracle's reading is pinned to torch's AdamW, a library implementation of
+# that rule: a multiplicative (1 - eta*lambda) shrink, applied before the
+# optimizer's own update and independent of it.
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("variant", ["malt", "malter"])
+def test_p14_zero_gradient_step_is_adamw_decay(variant):
+    import torch
+    shapes = [(5, 7), (7, 3)]
+    lr, lam = 3e-2, 0.1
+    W0 = [_rand(s, 140 + i) for i, s in enumerate(shapes)]
+    W, _ = oracle_step(W0, [np.zeros(s) for s in shapes], oracle_init(shapes, variant),
+                       OracleHparams(variant=variant, lr=lr, weight_decay=lam))
+    ps = [torch.tensor(w, dtype=torch.float64, requires_grad=True) for w in W0]
+    opt = torch.optim.AdamW(ps, lr=lr, weight_decay=lam)
+    for p in ps:
+        p.grad = torch.zeros_like(p)
+    opt.step()
+    for w, p in zip(W, ps):
+        np.testing.assert_allclose(w, p.detach().numpy(), rtol=1e-15, atol=0)
+
+
+@pytest.mark.parametrize("variant", ["malt", "malter"])
+def test_p14_decay_precedes_and_separates_from_the_update(variant):
+    shapes = [(6, 9), (9, 4)]
+    lr, lam = 2e-2, 0.1
+    W0 = [_rand(s, 150 + i) for i, s in enumerate(shapes)]
+    G = [[_rand(s, 160 + 10 * t + i, 1e-2) for i, s in enumerate(shapes)] for t in range(3)]
+    runs = {}
+    for wd in (0.0, lam):
+        st = oracle_init(shapes, variant)
+        W, steps = [w.copy() for w in W0], []
+        for t in range(3):
+            Wn, _ = oracle_step(W, G[t], st, OracleHparams(variant=variant, lr=lr, weight_decay=wd))
+            steps.append([wn - w for wn, w in zip(Wn, W)])
+            W = Wn
+        runs[wd] = (W, steps)
+    # The direction does not depend on W, so with decay each step adds exactly
+    # -eta*lambda*W_prev to the undecayed step; W_prev is the decayed iterate.
+    W_prev = [w.copy() for w in W0]
+    for t in range(3):
+        for i in range(len(shapes)):
+            np.testing.assert_allclose(runs[lam][1][t][i] - runs[0.0][1][t][i], -lr * lam * W_prev[i],
+                                       rtol=1e-9, atol=1e-15)
+        W_prev = [w + d for w, d in zip(W_prev, runs[lam][1][t])]
