@@ -63,7 +63,14 @@ constexpr int LOADS = 2 * OPER_BYTES / 1024 / NW;    // 1 KB direct loads per wa
 constexpr int EPI_F = NS_TILE + 4;                   // fp32 epilogue stage row (floats)
 constexpr int EPI_B = NS_TILE + 8;                   // bf16 epilogue stage row
 constexpr int EPI_BYTES = 64 * EPI_F * 4 + 2 * 64 * EPI_B * 2;
-constexpr int LDS_BYTES = RING_BYTES > EPI_BYTES ? RING_BYTES : EPI_BYTES;
+// Update epilogue: the whole bf16 output tile staged in LDS, rows padded by
+// 8 bytes so the 32 rows one 8-byte write touches land in distinct banks, then
+// the per-tile norm partials of the last iteration.
+constexpr int UPD_PITCH = NS_TILE * 2 + 8;
+constexpr int UPD_RED = NS_TILE * UPD_PITCH;
+constexpr int UPD_EPI_BYTES = UPD_RED + 2 * NW * 4;
+constexpr int LDS_BYTES_ = RING_BYTES > EPI_BYTES ? RING_BYTES : EPI_BYTES;
+constexpr int LDS_BYTES = LDS_BYTES_ > UPD_EPI_BYTES ? LDS_BYTES_ : UPD_EPI_BYTES;
 static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
 static_assert(H % 2 == 0, "sub-steps per stage must be even");
 static_assert(LOADS * NW * 1024 == 2 * OPER_BYTES, "loads must split evenly over the waves");
@@ -558,9 +565,14 @@ void ns_update_kernel(NsArgs args) {
 
   // ---------------------------------------------------------------- epilogue
   // acc[a][b][4g + e] = C(m, n + e), m = row0 + wr*TM + b*32 + (lane & 31),
-  // n = col0 + wc*TN + a*32 + 8g + 4*(lane >> 5): four consecutive bf16 per store.
-  const int mlane = row0 + wr * TM + (lane & 31);
-  const int nlane = col0 + wc * TN + 4 * (lane >> 5);
+  // n = col0 + wc*TN + a*32 + 8g + 4*(lane >> 5): four consecutive bf16 per
+  // lane.  They go to an LDS copy of the tile first; the tile then leaves in
+  // whole 512-byte rows (16 bytes per lane), not as 16-byte pieces of 32 rows.
+  const int ml0 = wr * TM + (lane & 31);          // tile-local row of b = 0
+  const int nl0 = wc * TN + 4 * (lane >> 5);      // tile-local column of a = g = 0
+  char* const sto = lds;
+  __syncthreads();   // every wave is done reading the operand ring
+  float o2 = 0.f, d2 = 0.f;
   if (!args.last) {
 #pragma unroll
     for (int b = 0; b < NB; ++b)
@@ -571,61 +583,75 @@ void ns_update_kernel(NsArgs args) {
           uint2 pk;
           pk.x = pack_bf16x2(sc * acc[a][b][4 * g + 0], sc * acc[a][b][4 * g + 1]);
           pk.y = pack_bf16x2(sc * acc[a][b][4 * g + 2], sc * acc[a][b][4 * g + 3]);
-          *reinterpret_cast<uint2*>(Xn + (size_t)(mlane + b * 32) * np + nlane + a * 32 + 8 * g) = pk;
+          *reinterpret_cast<uint2*>(sto + (ml0 + b * 32) * UPD_PITCH + (nl0 + a * 32 + 8 * g) * 2) = pk;
         }
-    return;
-  }
-  // Last iteration: also the per-tile sums of O^2 and (L O R)^2.  Canonical
-  // (m, n) is W(m, n) for wide and W(n, m) for tall matrices.
-  const float* const Lm = tall ? Rv : Lv;   // factor indexed by the canonical row
-  const float* const Ln = tall ? Lv : Rv;   // factor indexed by the canonical column
-  // (Lm O Ln)^2 = Lm^2 Ln^2 O^2: four squared row factors per lane, four
-  // squared column factors per (a, g).
-  float lm2[NB];
+  } else {
+    // Last iteration: also the per-tile sums of O^2 and (L O R)^2, from the
+    // rounded O.  Canonical (m, n) is W(m, n) for wide and W(n, m) for tall
+    // matrices.
+    const float* const Lm = tall ? Rv : Lv;   // factor indexed by the canonical row
+    const float* const Ln = tall ? Lv : Rv;   // factor indexed by the canonical column
+    // (Lm O Ln)^2 = Lm^2 Ln^2 O^2: four squared row factors per lane, four
+    // squared column factors per (a, g).
+    float lm2[NB];
 #pragma unroll
-  for (int b = 0; b < NB; ++b) {
-    const int m = mlane + b * 32;
-    const float l = m < mc ? Lm[m] : 0.f;
-    lm2[b] = l * l;
-  }
-  float o2 = 0.f, d2 = 0.f;
+    for (int b = 0; b < NB; ++b) {
+      const int m = row0 + ml0 + b * 32;
+      const float l = m < mc ? Lm[m] : 0.f;
+      lm2[b] = l * l;
+    }
 #pragma unroll
-  for (int a = 0; a < NA; ++a) {
+    for (int a = 0; a < NA; ++a) {
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int n = nlane + a * 32 + 8 * g;
-      float ln2[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float l = n + e < nc ? Ln[n + e] : 0.f;
-        ln2[e] = l * l;
-      }
-#pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        const int m = mlane + b * 32;
-        uint2 pk;
-        pk.x = pack_bf16x2(sc * acc[a][b][4 * g + 0], sc * acc[a][b][4 * g + 1]);
-        pk.y = pack_bf16x2(sc * acc[a][b][4 * g + 2], sc * acc[a][b][4 * g + 3]);
-        *reinterpret_cast<uint2*>(Xn + (size_t)m * np + n) = pk;
-        const float ov[4] = {bf16_lo(pk.x), bf16_hi(pk.x), bf16_lo(pk.y), bf16_hi(pk.y)};
-        float rowo = 0.f, rowd = 0.f;
+      for (int g = 0; g < 4; ++g) {
+        const int nl = nl0 + a * 32 + 8 * g;
+        const int n = col0 + nl;
+        float ln2[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float q = (n + e < nc) ? ov[e] * ov[e] : 0.f;   // zero padding contributes 0 anyway
-          rowo += q;
-          rowd += ln2[e] * q;
+          const float l = n + e < nc ? Ln[n + e] : 0.f;
+          ln2[e] = l * l;
         }
-        if (m < mc) {
-          o2 += rowo;
-          d2 += lm2[b] * rowd;
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+          const int m = row0 + ml0 + b * 32;
+          uint2 pk;
+          pk.x = pack_bf16x2(sc * acc[a][b][4 * g + 0], sc * acc[a][b][4 * g + 1]);
+          pk.y = pack_bf16x2(sc * acc[a][b][4 * g + 2], sc * acc[a][b][4 * g + 3]);
+          *reinterpret_cast<uint2*>(sto + (ml0 + b * 32) * UPD_PITCH + nl * 2) = pk;
+          const float ov[4] = {bf16_lo(pk.x), bf16_hi(pk.x), bf16_lo(pk.y), bf16_hi(pk.y)};
+          float rowo = 0.f, rowd = 0.f;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float q = (n + e < nc) ? ov[e] * ov[e] : 0.f;   // zero padding contributes 0 anyway
+            rowo += q;
+            rowd += ln2[e] * q;
+          }
+          if (m < mc) {
+            o2 += rowo;
+            d2 += lm2[b] * rowd;
+          }
         }
+        asm volatile("" ::: "memory");   // keep the column-factor loads of one (a, g) at a time
       }
-      asm volatile("" ::: "memory");   // keep the column-factor loads of one (a, g) at a time
     }
   }
-  // Deterministic per-tile sums for the graft norms.
   __syncthreads();
-  float* red = reinterpret_cast<float*>(lds);
+  // Copy-out: 256 rows x 32 chunks of 16 bytes; a wave writes two whole rows
+  // per store.  Each chunk is read as two 8-byte halves (rows are 8-byte
+  // aligned in the padded copy).
+  constexpr int CHUNKS = NS_TILE * NS_TILE * 2 / 16;
+#pragma unroll 4
+  for (int c = tid; c < CHUNKS; c += NT) {
+    const int row = c >> 5, ch = c & 31;
+    const char* src = sto + row * UPD_PITCH + ch * 16;
+    const uint2 lo = *reinterpret_cast<const uint2*>(src);
+    const uint2 hi = *reinterpret_cast<const uint2*>(src + 8);
+    *reinterpret_cast<uint4*>(Xn + (size_t)(row0 + row) * np + col0 + ch * 8) = make_uint4(lo.x, lo.y, hi.x, hi.y);
+  }
+  if (!args.last) return;
+  // Deterministic per-tile sums for the graft norms (LDS past the staged tile).
+  float* red = reinterpret_cast<float*>(lds + UPD_RED);
   o2 = wsum(o2);
   d2 = wsum(d2);
   if (lane == 0) {
