@@ -60,17 +60,20 @@ constexpr int OPER_BYTES = NS_TILE * BK * 2;         // one operand tile of one 
 constexpr int STAGE_BYTES = 2 * OPER_BYTES;
 constexpr int RING_BYTES = STAGES * STAGE_BYTES;
 constexpr int LOADS = 2 * OPER_BYTES / 1024 / NW;    // 1 KB direct loads per wave per stage
-constexpr int EPI_F = NS_TILE + 4;                   // fp32 epilogue stage row (floats)
-constexpr int EPI_B = NS_TILE + 8;                   // bf16 epilogue stage row
-constexpr int EPI_BYTES = 64 * EPI_F * 4 + 2 * 64 * EPI_B * 2;
-// Update epilogue: the whole bf16 output tile staged in LDS, rows padded by
-// 8 bytes so the 32 rows one 8-byte write touches land in distinct banks, then
-// the per-tile norm partials of the last iteration.
-constexpr int UPD_PITCH = NS_TILE * 2 + 8;
+// Epilogues stage a whole bf16 output tile in LDS and write it out in
+// 512-byte rows.  A tile written column-wise (each lane: four consecutive rows
+// of one column, 8 bytes into one staged row) uses rows padded by 8 bytes, so
+// the 32 staged rows of one write land in distinct banks; a tile written
+// row-wise (each lane: four consecutive columns) uses rows padded by 64 bytes.
+// The update keeps its per-tile norm partials past the staged tile.
+constexpr int ST_PITCH_T = NS_TILE * 2 + 8;
+constexpr int ST_PITCH_R = NS_TILE * 2 + 64;
+constexpr int UPD_PITCH = ST_PITCH_T;
 constexpr int UPD_RED = NS_TILE * UPD_PITCH;
 constexpr int UPD_EPI_BYTES = UPD_RED + 2 * NW * 4;
-constexpr int LDS_BYTES_ = RING_BYTES > EPI_BYTES ? RING_BYTES : EPI_BYTES;
-constexpr int LDS_BYTES = LDS_BYTES_ > UPD_EPI_BYTES ? LDS_BYTES_ : UPD_EPI_BYTES;
+constexpr int SYM_EPI_BYTES = NS_TILE * ST_PITCH_R;
+constexpr int EPI_BYTES = UPD_EPI_BYTES > SYM_EPI_BYTES ? UPD_EPI_BYTES : SYM_EPI_BYTES;
+constexpr int LDS_BYTES = RING_BYTES > EPI_BYTES ? RING_BYTES : EPI_BYTES;
 static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
 static_assert(H % 2 == 0, "sub-steps per stage must be even");
 static_assert(LOADS * NW * 1024 == 2 * OPER_BYTES, "loads must split evenly over the waves");
@@ -345,101 +348,143 @@ void ns_gemm_sym_kernel(NsArgs args) {
       });
 
   // ---------------------------------------------------------------- epilogue
-  // Four rounds; round i stages rows {wr*TM + i*32 + [0,32)} of both wave rows
-  // (64 tile rows x 256 cols, fp32) in LDS.  Pass 1 reads 8 consecutive
-  // columns per thread, applies the phase's epilogue, writes bf16 rows and
-  // keeps the bf16 values in LDS; pass 2 writes the mirrored tile from there.
-  // Staged row lr is tile row (lr >> 5) * TM + i * 32 + (lr & 31).
-  float* stf = reinterpret_cast<float*>(lds);                       // [64][EPI_F]
-  bf16_t* stb = reinterpret_cast<bf16_t*>(lds + 64 * EPI_F * 4);    // [64][EPI_B]
-  bf16_t* stl = stb + 64 * EPI_B;                                   // [64][EPI_B] (split low part)
+  // acc[i][j][4g + e] = C(r, c): tile row r = wr*TM + i*32 + 8g + 4*(lane >> 5)
+  // + e, tile column c = wc*TN + j*32 + (lane & 31), so each lane holds four
+  // consecutive rows of one column.  The final bf16 values are formed in
+  // registers; the tile then leaves through LDS twice in whole rows: first
+  // transposed (the mirror tile C^T, or the tile itself on the diagonal),
+  // then, for off-diagonal tiles, as is after a 4 x 4 transpose inside each
+  // lane quad.
+  const bool poly = phase == PH_POLY;
   const bool mirror = t.ti != t.tj;
   const float sc = sig * sig;
   // Split B': the low part bf16(v - hi) goes mp columns to the right.
-  const int lo_off = (phase == PH_POLY && split) ? mp : 0;
-  bf16_t* out = (phase == PH_GRAM) ? Am : Bm;
+  const int lo_off = (poly && split) ? mp : 0;
+  bf16_t* const out = poly ? Bm : Am;
   const int ldo = lo_off ? 2 * mp : mp;
-  const bool poly = phase == PH_POLY;
+  const int rl0 = wr * TM + 4 * (lane >> 5);   // tile row of i = g = e = 0
+  const int cl0 = wc * TN + (lane & 31);       // tile column of j = 0
 
-  constexpr int P1ROWS = NT / 32;           // pass 1: 32 threads per staged row, 8 columns each
-  const int p1c = (tid & 31) * 8, p1r = tid >> 5;
-  constexpr int P2COLS = NT / 4;            // pass 2: 4 threads per output column, 8 rows each
-  const int p2c = tid >> 2, p2s = (tid & 3) * 8;
-
+  __syncthreads();   // every wave is done reading the operand ring
+  if (poly) {
+    // B' = a I + b A + c A A^T takes A(r, c) at each accumulator position.
+    // A's tile goes to LDS as 256 rows in the [k][n] layout (direct loads),
+    // and each lane reads its four rows of one column with one transposed
+    // read per (i, j, g).
+    const i32x4 rsA = buf_rsrc(Am);
 #pragma unroll
-  for (int i = 0; i < I; ++i) {
-    __syncthreads();   // the ring / previous round's readers are done with LDS
-#pragma unroll
-    for (int j = 0; j < J; ++j)
-#pragma unroll
-      for (int g = 0; g < 4; ++g)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int lr = wr * 32 + g * 8 + (lane >> 5) * 4 + e;
-          const int lc = wc * TN + j * 32 + (lane & 31);
-          stf[lr * EPI_F + lc] = acc[i][j][4 * g + e];
-        }
-    __syncthreads();
-    for (int k = 0; k < 64 / P1ROWS; ++k) {
-      const int lr = p1r + P1ROWS * k;
-      const int R = row0 + (lr >> 5) * TM + i * 32 + (lr & 31);
-      const int C = col0 + p1c;
-      const float4 a0 = *reinterpret_cast<const float4*>(stf + lr * EPI_F + p1c);
-      const float4 a1 = *reinterpret_cast<const float4*>(stf + lr * EPI_F + p1c + 4);
-      float v[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
-      if (poly) {
-        // B' = a I + b A + c A A^T with the same bf16 A the product used.
-        const uint4 q = *reinterpret_cast<const uint4*>(Am + (size_t)R * mp + C);
-        const uint32_t qw[4] = {q.x, q.y, q.z, q.w};
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float av = bf2f_((bf16_t)((qw[e >> 1] >> (16 * (e & 1))) & 0xffffu));
-          v[e] = args.b * av + args.c * v[e] + (R == C + e ? args.a : 0.f);
-        }
-      }
-      uint32_t hw[4], lw[4];
-#pragma unroll
-      for (int e = 0; e < 8; e += 2) {
-        const float v0 = sc * v[e], v1 = sc * v[e + 1];
-        const uint32_t hp = pack_bf16x2(v0, v1);
-        hw[e >> 1] = hp;
-        stb[lr * EPI_B + p1c + e] = (bf16_t)(hp & 0xffffu);
-        stb[lr * EPI_B + p1c + e + 1] = (bf16_t)(hp >> 16);
-        if (lo_off) {
-          const uint32_t lp = pack_bf16x2(v0 - bf16_lo(hp), v1 - bf16_hi(hp));
-          lw[e >> 1] = lp;
-          stl[lr * EPI_B + p1c + e] = (bf16_t)(lp & 0xffffu);
-          stl[lr * EPI_B + p1c + e + 1] = (bf16_t)(lp >> 16);
-        }
-      }
-      *reinterpret_cast<uint4*>(out + (size_t)R * ldo + C) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
-      if (lo_off)
-        *reinterpret_cast<uint4*>(out + (size_t)R * ldo + lo_off + C) = make_uint4(lw[0], lw[1], lw[2], lw[3]);
+    for (int it = 0; it < NS_TILE * NS_TILE * 2 / (16 * NT); ++it) {
+      const int c = tid + NT * it;                // 16-byte chunk of the tile
+      const int row = c >> 5, pc = c & 31;        // physical chunk pc holds logical chunk pc ^ 4 (row & 3)
+      const int lc = pc ^ (4 * (row & 3));
+      dma16(rsA, (uint32_t)(((size_t)(row0 + row) * mp + col0 + lc * 8) * 2), 0u,
+            lds_u32(lds + (c - lane) * 16));
     }
-    if (mirror) {
-      __syncthreads();
+    wait_vm_c<0>();
+    __syncthreads();
+  }
+  uint2 hv[I][J][4];
+  {
+    const int r = (lane & 15) >> 2, q = lane & 3;
 #pragma unroll
-      for (int q = 0; q < NS_TILE / P2COLS; ++q) {
-        const int lc = p2c + P2COLS * q;
-        const int C = col0 + lc;
+    for (int i = 0; i < I; ++i)
 #pragma unroll
-        for (int band = 0; band < 2; ++band) {
-          const int lr0 = band * 32 + p2s;
-          const int R = row0 + band * TM + i * 32 + p2s;
-          uint32_t hw[4];
+      for (int j = 0; j < J; ++j)
 #pragma unroll
-          for (int e = 0; e < 8; e += 2)
-            hw[e >> 1] = (uint32_t)stb[(lr0 + e) * EPI_B + lc] | ((uint32_t)stb[(lr0 + e + 1) * EPI_B + lc] << 16);
-          *reinterpret_cast<uint4*>(out + (size_t)C * ldo + R) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+        for (int g = 0; g < 4; ++g) {
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * g + e];
+          if (poly) {
+            const int k0 = rl0 + i * 32 + 8 * g;
+            const int n0 = wc * TN + j * 32 + 16 * ((lane >> 4) & 1);
+            const i16x4 av = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(lds + swz_kn(k0 + r, n0 + 4 * q)));
+            const int R = row0 + k0, C = col0 + cl0 + j * 32;
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              v[e] = args.b * bf2f_((bf16_t)av[e]) + args.c * v[e] + (R + e == C ? args.a : 0.f);
+          }
+          hv[i][j][g].x = pack_bf16x2(sc * v[0], sc * v[1]);
+          hv[i][j][g].y = pack_bf16x2(sc * v[2], sc * v[3]);
           if (lo_off) {
-#pragma unroll
-            for (int e = 0; e < 8; e += 2)
-              hw[e >> 1] = (uint32_t)stl[(lr0 + e) * EPI_B + lc] | ((uint32_t)stl[(lr0 + e + 1) * EPI_B + lc] << 16);
-            *reinterpret_cast<uint4*>(out + (size_t)C * ldo + lo_off + R) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+            // Keep the low parts in acc (its values are no longer needed).
+            acc[i][j][4 * g + 0] = sc * v[0] - bf16_lo(hv[i][j][g].x);
+            acc[i][j][4 * g + 1] = sc * v[1] - bf16_hi(hv[i][j][g].x);
+            acc[i][j][4 * g + 2] = sc * v[2] - bf16_lo(hv[i][j][g].y);
+            acc[i][j][4 * g + 3] = sc * v[3] - bf16_hi(hv[i][j][g].y);
           }
         }
-      }
+  }
+
+  // Writes one set of values (hi, or the split low part at column offset
+  // off): the transposed staging first, then the row-wise one.
+  auto emit = [&](int off) {
+    constexpr int CHUNKS = NS_TILE * NS_TILE * 2 / 16;
+    __syncthreads();   // LDS free (A's tile read, or the previous copy-out done)
+#pragma unroll
+    for (int i = 0; i < I; ++i)
+#pragma unroll
+      for (int j = 0; j < J; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          *reinterpret_cast<uint2*>(lds + (cl0 + j * 32) * ST_PITCH_T + (rl0 + i * 32 + 8 * g) * 2) = hv[i][j][g];
+    __syncthreads();
+    // Staged row x is tile column x: it goes to row col0 + x (the mirror
+    // tile; on the diagonal, col0 = row0 and it is the tile itself).
+#pragma unroll 4
+    for (int c = tid; c < CHUNKS; c += NT) {
+      const int row = c >> 5, ch = c & 31;
+      const char* src = lds + row * ST_PITCH_T + ch * 16;
+      const uint2 lo = *reinterpret_cast<const uint2*>(src);
+      const uint2 hi = *reinterpret_cast<const uint2*>(src + 8);
+      *reinterpret_cast<uint4*>(out + (size_t)(col0 + row) * ldo + off + row0 + ch * 8) =
+          make_uint4(lo.x, lo.y, hi.x, hi.y);
     }
+    if (!mirror) return;
+    __syncthreads();
+    // 4 x 4 transpose of 16-bit values inside each lane quad: lane p of the
+    // quad ends with row p of the quad's four rows, its four columns.
+    const int p = lane & 3;
+#pragma unroll
+    for (int i = 0; i < I; ++i)
+#pragma unroll
+      for (int j = 0; j < J; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const uint32_t A0 = hv[i][j][g].x, B0 = hv[i][j][g].y;   // rows (0,1), (2,3) of column p
+          const uint32_t A1 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)A0, 0xB1, 0xF, 0xF, true);   // lane p ^ 1
+          const uint32_t B1 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)B0, 0xB1, 0xF, 0xF, true);
+          // Even lanes: row 0 (A) / row 2 (B) at columns p, p+1; odd lanes:
+          // row 1 / row 3 at columns p-1, p.
+          const uint32_t nA = (p & 1) ? ((A1 >> 16) | (A0 & 0xffff0000u)) : ((A0 & 0xffffu) | (A1 << 16));
+          const uint32_t nB = (p & 1) ? ((B1 >> 16) | (B0 & 0xffff0000u)) : ((B0 & 0xffffu) | (B1 << 16));
+          const uint32_t S = (p < 2) ? nB : nA;
+          const uint32_t S2 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)S, 0x4E, 0xF, 0xF, true);   // lane p ^ 2
+          const uint2 rowv = (p < 2) ? make_uint2(nA, S2) : make_uint2(S2, nB);
+          const int rr = rl0 + i * 32 + 8 * g + p;
+          const int cc = wc * TN + j * 32 + ((lane & 31) & ~3);
+          *reinterpret_cast<uint2*>(lds + rr * ST_PITCH_R + cc * 2) = rowv;
+        }
+    __syncthreads();
+#pragma unroll 4
+    for (int c = tid; c < CHUNKS; c += NT) {
+      const int row = c >> 5, ch = c & 31;
+      *reinterpret_cast<uint4*>(out + (size_t)(row0 + row) * ldo + off + col0 + ch * 8) =
+          *reinterpret_cast<const uint4*>(lds + row * ST_PITCH_R + ch * 16);
+    }
+  };
+  emit(0);
+  if (lo_off) {
+#pragma unroll
+    for (int i = 0; i < I; ++i)
+#pragma unroll
+      for (int j = 0; j < J; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          hv[i][j][g].x = pack_bf16x2(acc[i][j][4 * g + 0], acc[i][j][4 * g + 1]);
+          hv[i][j][g].y = pack_bf16x2(acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+        }
+    emit(lo_off);
   }
 }
 
