@@ -36,6 +36,7 @@ namespace malt {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 #ifndef MALT_NS_BK
 #define MALT_NS_BK 64
@@ -692,7 +693,10 @@ void ns_update_kernel(NsArgs args) {
     const char* src = sto + row * UPD_PITCH + ch * 16;
     const uint2 lo = *reinterpret_cast<const uint2*>(src);
     const uint2 hi = *reinterpret_cast<const uint2*>(src + 8);
-    *reinterpret_cast<uint4*>(Xn + (size_t)(row0 + row) * np + col0 + ch * 8) = make_uint4(lo.x, lo.y, hi.x, hi.y);
+    // Streaming store: the next kernel reads X' from another XCD's L2 anyway,
+    // and the operand panels keep this one.
+    const u32x4 v = {lo.x, lo.y, hi.x, hi.y};
+    __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(Xn + (size_t)(row0 + row) * np + col0 + ch * 8));
   }
   if (!args.last) return;
   // Deterministic per-tile sums for the graft norms (LDS past the staged tile).
