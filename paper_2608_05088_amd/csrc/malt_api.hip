@@ -45,12 +45,14 @@ inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct MatPlan {
   int64_t m, n, mc, nc, mp, np;
-  bool tall, split;
+  bool tall, split, small;
+  int64_t sm_gchunks;                  // fp32 path: Gram partials
   int64_t k1_ct, k1_rt, k2_tr, k2_tc, k2_tiles, upd_tiles, sym_tiles;
   // offsets
   int64_t st_M, st_l, st_r, st_nu;     // floats from state base
   size_t ws_scal, ws_Lv, ws_Rv, ws_rowpart, ws_colpart, ws_k2part, ws_gpart;
   size_t ws_X[2], ws_A, ws_B;
+  size_t ws_Xs[2], ws_Ap, ws_Bs;       // fp32 path only
   // algorithmic cost
   double ns_flops_sym_per_iter;        // 3 mc^2 nc + mc^3 (symmetric minimum)
 };
@@ -60,7 +62,9 @@ struct Layout {
   size_t state_bytes = 0, ws_bytes = 0;
   size_t ws_desc = 0, ws_ptrs = 0;
   size_t ws_t_ew = 0, ws_t_fin = 0, ws_t_k2 = 0, ws_t_sym = 0, ws_t_upd = 0;
+  size_t ws_t_smg = 0, ws_t_smp = 0, ws_t_smu = 0;
   int64_t n_ew = 0, n_fin = 0, n_k2 = 0, n_sym = 0, n_upd = 0;
+  int64_t n_smg = 0, n_smp = 0, n_smu = 0;   // fp32 Newton-Schulz lists
 };
 
 malt_status_t check_shapes(const malt_shape_t* shapes, int32_t n) {
@@ -100,20 +104,30 @@ Layout make_layout(const malt_shape_t* shapes, int32_t n, malt_variant_t variant
     p.tall = p.m > p.n;
     p.mc = std::min(p.m, p.n); p.nc = std::max(p.m, p.n);
     p.mp = pad_to(p.mc, NS_TILE); p.np = pad_to(p.nc, NS_TILE);
-    p.split = p.mc <= NS_SPLIT_MAX;
+    p.small = p.mc <= NS_SMALL_MAX;
+    p.split = !p.small && p.mc <= NS_SPLIT_MAX;
+    p.sm_gchunks = p.small ? cdiv(p.np, SM_CH_G) : 0;
     p.k1_ct = cdiv(p.n, EW_TC); p.k1_rt = cdiv(p.m, EW_TR);
     const int64_t wrows_p = p.tall ? p.np : p.mp, wcols_p = p.tall ? p.mp : p.np;
     p.k2_tr = wrows_p / K2_T; p.k2_tc = wcols_p / K2_T;
     p.k2_tiles = p.k2_tr * p.k2_tc;
     const int64_t T = p.mp / NS_TILE;
-    p.sym_tiles = T * (T + 1) / 2;
-    p.upd_tiles = T * (p.np / NS_TILE);
+    // fp32 path: no matrix-core tiles; the update's partial slots are its
+    // column chunks.
+    p.sym_tiles = p.small ? 0 : T * (T + 1) / 2;
+    p.upd_tiles = p.small ? p.np / SM_CH_U : T * (p.np / NS_TILE);
     p.ns_flops_sym_per_iter = 3.0 * double(p.mc) * p.mc * p.nc + double(p.mc) * p.mc * p.mc;
     L.n_ew += p.k1_rt * p.k1_ct;
     L.n_fin += cdiv(p.m, NTHREADS) + cdiv(p.n, NTHREADS);
     L.n_k2 += p.k2_tiles;
-    L.n_sym += p.sym_tiles;
-    L.n_upd += p.upd_tiles;
+    if (p.small) {
+      L.n_smg += p.sm_gchunks;
+      L.n_smp += 1;
+      L.n_smu += p.upd_tiles;
+    } else {
+      L.n_sym += p.sym_tiles;
+      L.n_upd += p.upd_tiles;
+    }
   }
   size_t off = 0;
   auto take = [&](size_t bytes) { const size_t o = off; off = align256(off + bytes); return o; };
@@ -124,6 +138,9 @@ Layout make_layout(const malt_shape_t* shapes, int32_t n, malt_variant_t variant
   L.ws_t_k2 = take(sizeof(Tile) * L.n_k2);
   L.ws_t_sym = take(sizeof(Tile) * L.n_sym);
   L.ws_t_upd = take(sizeof(Tile) * L.n_upd);
+  L.ws_t_smg = take(sizeof(Tile) * L.n_smg);
+  L.ws_t_smp = take(sizeof(Tile) * L.n_smp);
+  L.ws_t_smu = take(sizeof(Tile) * L.n_smu);
   for (int32_t i = 0; i < n; ++i) {
     MatPlan& p = L.mats[i];
     p.ws_scal = take(sizeof(double) * MAT_SCALARS);
@@ -136,6 +153,13 @@ Layout make_layout(const malt_shape_t* shapes, int32_t n, malt_variant_t variant
     for (int b = 0; b < 2; ++b) p.ws_X[b] = take(2 * size_t(p.mp) * p.np);
     p.ws_A = take(2 * size_t(p.mp) * p.mp);
     p.ws_B = take(2 * size_t(p.mp) * p.mp * (p.split ? 2 : 1));
+    if (p.small) {
+      for (int b = 0; b < 2; ++b) p.ws_Xs[b] = take(4 * size_t(p.mc) * p.np);
+      p.ws_Ap = take(4 * size_t(p.sm_gchunks) * NS_SMALL_MAX * NS_SMALL_MAX);
+      p.ws_Bs = take(4 * size_t(NS_SMALL_MAX) * NS_SMALL_MAX);
+    } else {
+      p.ws_Xs[0] = p.ws_Xs[1] = p.ws_Ap = p.ws_Bs = 0;
+    }
   }
   L.ws_bytes = off;
   return L;
@@ -254,11 +278,17 @@ void fill_desc(const malt_plan* p, std::vector<MatDesc>& D) {
     d.A = reinterpret_cast<bf16_t*>(w + q.ws_A);
     d.B = reinterpret_cast<bf16_t*>(w + q.ws_B);
     d.scal = reinterpret_cast<double*>(w + q.ws_scal);
+    d.small = q.small ? 1 : 0;
+    d.sm_gchunks = int32_t(q.sm_gchunks);
+    for (int b = 0; b < 2; ++b) d.Xs[b] = q.small ? reinterpret_cast<float*>(w + q.ws_Xs[b]) : nullptr;
+    d.Ap = q.small ? reinterpret_cast<float*>(w + q.ws_Ap) : nullptr;
+    d.Bs = q.small ? reinterpret_cast<float*>(w + q.ws_Bs) : nullptr;
   }
 }
 
 void build_tiles(const malt_plan* p, std::vector<Tile>& ew, std::vector<Tile>& fin, std::vector<Tile>& k2,
-                 std::vector<Tile>& sym, std::vector<Tile>& upd) {
+                 std::vector<Tile>& sym, std::vector<Tile>& upd, std::vector<Tile>& smg, std::vector<Tile>& smp,
+                 std::vector<Tile>& smu) {
   const std::vector<int32_t> ord = cost_order(p->L);
   for (int32_t i : ord) {
     const MatPlan& q = p->L.mats[i];
@@ -269,6 +299,12 @@ void build_tiles(const malt_plan* p, std::vector<Tile>& ew, std::vector<Tile>& f
     int32_t idx = 0;
     for (int32_t ti = 0; ti < q.k2_tr; ++ti)
       for (int32_t tj = 0; tj < q.k2_tc; ++tj) k2.push_back({i, ti, tj, idx++});
+    if (q.small) {
+      for (int32_t c = 0; c < q.sm_gchunks; ++c) smg.push_back({i, c, 0, 0});
+      smp.push_back({i, 0, 0, 0});
+      for (int32_t c = 0; c < q.upd_tiles; ++c) smu.push_back({i, c, 0, c});
+      continue;
+    }
     const int32_t T = int32_t(q.mp / NS_TILE), TN = int32_t(q.np / NS_TILE);
     idx = 0;
     for (int32_t ti = 0; ti < T; ++ti)
@@ -345,11 +381,11 @@ malt_status_t malt_init_state(malt_plan_t** out, const malt_shape_t* shapes, int
 
   std::vector<MatDesc> D;
   fill_desc(p, D);
-  std::vector<Tile> ew, fin, k2, sym, upd;
-  build_tiles(p, ew, fin, k2, sym, upd);
+  std::vector<Tile> ew, fin, k2, sym, upd, smg, smp, smu;
+  build_tiles(p, ew, fin, k2, sym, upd, smg, smp, smu);
 
   // Stage every table in one pinned buffer laid out like the workspace head.
-  const size_t head = p->L.ws_t_upd + sizeof(Tile) * upd.size();
+  const size_t head = p->L.ws_t_smu + sizeof(Tile) * smu.size();
   void* h = nullptr;
   hipError_t e = hipHostMalloc(&h, head, hipHostMallocDefault);
   if (e != hipSuccess) { delete p; return hip_fail(e, "hipHostMalloc"); }
@@ -361,6 +397,9 @@ malt_status_t malt_init_state(malt_plan_t** out, const malt_shape_t* shapes, int
   memcpy(hc + p->L.ws_t_k2, k2.data(), sizeof(Tile) * k2.size());
   memcpy(hc + p->L.ws_t_sym, sym.data(), sizeof(Tile) * sym.size());
   memcpy(hc + p->L.ws_t_upd, upd.data(), sizeof(Tile) * upd.size());
+  memcpy(hc + p->L.ws_t_smg, smg.data(), sizeof(Tile) * smg.size());
+  memcpy(hc + p->L.ws_t_smp, smp.data(), sizeof(Tile) * smp.size());
+  memcpy(hc + p->L.ws_t_smu, smu.data(), sizeof(Tile) * smu.size());
 
   e = hipMemsetAsync(p->ws, 0, p->L.ws_bytes, s);
   if (e == hipSuccess) e = hipMemcpyAsync(p->ws, hc, head, hipMemcpyHostToDevice, s);
@@ -489,14 +528,27 @@ malt_status_t malt_step(malt_plan_t* p, float* const* params, const float* const
       na.first = it == 0;
       na.last = it == hp->ns_steps - 1;
       na.src = it & 1;
-      na.tiles = tiles_at(p->L.ws_t_sym); na.ntiles = int32_t(p->L.n_sym);
-      na.phase = PH_GRAM;
-      MALT_LAUNCH(4, launch_ns_gemm(na, s));
-      na.phase = PH_POLY;
-      MALT_LAUNCH(5, launch_ns_gemm(na, s));
-      na.tiles = tiles_at(p->L.ws_t_upd); na.ntiles = int32_t(p->L.n_upd);
-      na.phase = PH_UPDATE;
-      MALT_LAUNCH(6, launch_ns_gemm(na, s));
+      if (p->L.n_sym > 0) {   // matrix-core path
+        na.tiles = tiles_at(p->L.ws_t_sym); na.ntiles = int32_t(p->L.n_sym);
+        na.phase = PH_GRAM;
+        MALT_LAUNCH(4, launch_ns_gemm(na, s));
+        na.phase = PH_POLY;
+        MALT_LAUNCH(5, launch_ns_gemm(na, s));
+        na.tiles = tiles_at(p->L.ws_t_upd); na.ntiles = int32_t(p->L.n_upd);
+        na.phase = PH_UPDATE;
+        MALT_LAUNCH(6, launch_ns_gemm(na, s));
+      }
+      if (p->L.n_smp > 0) {   // fp32 path of the small matrices
+        na.tiles = tiles_at(p->L.ws_t_smg); na.ntiles = int32_t(p->L.n_smg);
+        na.phase = PH_GRAM;
+        MALT_LAUNCH(4, launch_small_ns(na, s));
+        na.tiles = tiles_at(p->L.ws_t_smp); na.ntiles = int32_t(p->L.n_smp);
+        na.phase = PH_POLY;
+        MALT_LAUNCH(5, launch_small_ns(na, s));
+        na.tiles = tiles_at(p->L.ws_t_smu); na.ntiles = int32_t(p->L.n_smu);
+        na.phase = PH_UPDATE;
+        MALT_LAUNCH(6, launch_small_ns(na, s));
+      }
     }
     MALT_LAUNCH(7, launch_graft_scalars(ea, n, s));
     ea.tiles = tiles_at(p->L.ws_t_ew); ea.ntiles = int32_t(p->L.n_ew);

@@ -24,6 +24,12 @@ constexpr int NS_BK = 64;
 constexpr int NS_SPLIT_MAX = 128;
 // Threads of every workgroup.
 constexpr int NTHREADS = 256;
+// Matrices whose short side is at most this run Newton-Schulz in fp32 (X, A
+// and B' kept in fp32): Gram partials over SM_CH_G columns per workgroup,
+// updates over SM_CH_U columns (one per thread).
+constexpr int NS_SMALL_MAX = 32;
+constexpr int SM_CH_G = 4096;
+constexpr int SM_CH_U = 256;
 
 typedef uint16_t bf16_t;   // bf16 storage
 
@@ -77,6 +83,12 @@ struct MatDesc {
   bf16_t* A;           // mp x mp  (Gram / A)
   bf16_t* B;           // mp x mp, or mp x 2mp [hi | lo] when split (b A + c A^2)
   double* scal;        // MAT_SCALARS
+  // fp32 Newton-Schulz (short side <= NS_SMALL_MAX); null otherwise
+  int32_t small;       // 1: this matrix takes the fp32 path
+  int32_t sm_gchunks;  // Gram partial count
+  float* Xs[2];        // canonical mc x np fp32 iterate (row pitch np)
+  float* Ap;           // [sm_gchunks][32][32] Gram partials
+  float* Bs;           // [32][32] B'
 };
 
 // Per-step caller pointers; vec = 1 when W, G and M rows allow 16-byte access.
@@ -92,6 +104,8 @@ struct PtrPair {
 //   preconditioner finalise: (mat, 0 = rows | 1 = cols, chunk, -)
 //   scale+convert: (mat, row tile, col tile, partial slot)
 //   NS: (mat, tile row, tile col, partial slot)
+//   fp32 NS: Gram (mat, chunk, -, -), polynomial (mat, -, -, -),
+//            update (mat, chunk, -, partial slot)
 struct Tile {
   int32_t mat, ti, tj, idx;
 };
@@ -133,6 +147,7 @@ hipError_t launch_norm_scalars(const EwArgs& a, int32_t nmat, hipStream_t s);
 hipError_t launch_graft_scalars(const EwArgs& a, int32_t nmat, hipStream_t s);
 hipError_t launch_backmap_write(const EwArgs& a, hipStream_t s);
 hipError_t launch_ns_gemm(const NsArgs& a, hipStream_t s);
+hipError_t launch_small_ns(const NsArgs& a, hipStream_t s);
 
 // Map a workgroup id to a work index so that the workgroups that land on one
 // XCD (dispatched round-robin over 8 XCDs) take a contiguous run of the work

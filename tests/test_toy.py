@@ -74,7 +74,7 @@ def test_libmalt_runs_the_toy():
 
 
 @pytest.mark.gpu
-@pytest.mark.parametrize("kappa", [10.0])
+@pytest.mark.parametrize("kappa", [10.0, 1e3, 1e4])
 def test_libmalt_toy_steps_match_the_oracle(kappa):
     """Three MALT steps on the 5 x 5 toy, the gradients taken along the GPU's
     own trajectory and fed to the oracle as well.  (At kappa = 1e3 the
