@@ -22,7 +22,9 @@
  * coefficients): X = Mt/(||Mt||_F + ns_eps) on the orientation with
  * rows <= cols, then ns_steps times  A = X X^T,  B = ns_b A + ns_c A A,
  * X <- ns_a X + B X.  It runs in bf16 on the matrix cores with fp32
- * accumulation; everything else is fp32 with fp64 scalar combines.
+ * accumulation; matrices whose shorter side is at most 32 run it in fp32
+ * instead (only the final O is rounded to bf16).  Everything else is fp32
+ * with fp64 scalar combines.
  *
  * Conventions shared by every entry point
  *  - Matrices are dense, row-major float32, `rows x cols`, 1 <= rows, cols <= 2^20,
@@ -100,8 +102,9 @@ typedef struct malt_plan malt_plan_t;
  *    [M_0 .. M_{n-1} | l_0 .. l_{n-1} | r_0 .. r_{n-1} | nu_0 .. nu_{n-1}],
  *    M_i row-major rows x cols; malt_state_layout() gives the offsets.
  *  workspace_bytes: scratch for the preconditioner vectors, reduction
- *    partials, the bf16 Newton-Schulz buffers (padded to multiples of 256)
- *    and the per-matrix scalar table.  Must be 256-byte aligned. */
+ *    partials, the bf16 Newton-Schulz buffers (padded to multiples of 256),
+ *    the fp32 Newton-Schulz buffers of matrices with a short side of at most
+ *    32, and the per-matrix scalar table.  Must be 256-byte aligned. */
 malt_status_t malt_state_size(const malt_shape_t* shapes, int32_t n, malt_variant_t variant,
                               size_t* state_bytes, size_t* workspace_bytes);
 
