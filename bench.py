@@ -172,7 +172,7 @@ def cpu_baseline(w, layers: int):
         pass
     return {"value": total_s * 1e3, "unit": "ms per step (extrapolated per shape)", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"one oracle step on {layers} matrix of each shape ({', '.join(sample_desc)}), "
+            "sample": f"one oracle step on {layers} matrices of each shape ({', '.join(sample_desc)}), "
                       f"{sampled_s:.1f} s of CPU time, scaled by shape counts to all {len(shapes)} matrices",
             "host_cpus": os.cpu_count(), "affinity_cpus": len(os.sched_getaffinity(0)), "cpu_model": cpu_model,
             "blas": ", ".join(f"{p.get('internal_api')} {p.get('version')}" for p in blas)}
