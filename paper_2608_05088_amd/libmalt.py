@@ -166,7 +166,10 @@ class Plan:
         import torch
         self.shapes: List[Tuple[int, int]] = [(int(m), int(n)) for m, n in shapes]
         self.variant = variant
-        self.device = torch.device(device if device is not None else "cuda")
+        dev = torch.device(device if device is not None else "cuda")
+        if dev.type == "cuda" and dev.index is None:
+            dev = torch.device("cuda", torch.cuda.current_device())
+        self.device = dev
         sb, wb = malt_state_size(self.shapes, variant)
         self.state_bytes, self.workspace_bytes = sb, wb
         if state is None:
@@ -186,9 +189,27 @@ class Plan:
     # -- stepping ----------------------------------------------------------------
     def step(self, params: Sequence, grads: Sequence, hp: Optional[malt_hparams_t] = None,
              stream=None) -> None:
+        import torch
         n = len(self.shapes)
         if len(params) != n or len(grads) != n:
             raise ValueError(f"expected {n} params and grads")
+        # The C ABI sees raw pointers: check here what it cannot (dtype,
+        # layout, device, shape), so a wrong tensor fails instead of being read
+        # as float32 rows.
+        for i, (p, g) in enumerate(zip(params, grads)):
+            for what, x in (("param", p), ("grad", g)):
+                if (x.dtype != torch.float32 or not x.is_contiguous() or x.device != self.device
+                        or tuple(x.shape) != self.shapes[i]):
+                    raise ValueError(f"matrix {i}: {what} must be a contiguous float32 tensor of shape "
+                                     f"{self.shapes[i]} on {self.device} (got {x.dtype}, {tuple(x.shape)}, "
+                                     f"{x.device}, contiguous={x.is_contiguous()})")
+        self._step_ptrs(params, grads, hp, stream)
+
+    def _step_ptrs(self, params: Sequence, grads: Sequence, hp: Optional[malt_hparams_t] = None,
+                   stream=None) -> None:
+        """malt_step on the tensors' data pointers, without the checks of step():
+        only the C library's own validation applies."""
+        n = len(self.shapes)
         P = (c_void_p * n)(*[c_void_p(p.data_ptr()) for p in params])
         G = (c_void_p * n)(*[c_void_p(g.data_ptr()) for g in grads])
         hp = hp if hp is not None else hparams_default()

@@ -88,8 +88,10 @@ def test_errors_leave_state_untouched():
         plan.step(W, G)
     assert e.value.status == lm.MALT_ERR_STATE_MISMATCH
     plan._c_shapes[0].rows = 64
+    with pytest.raises(ValueError):
+        plan.step([W[0], W[0]], G)            # matrix 1 gets a tensor of another shape
     with pytest.raises(lm.MaltError) as e:
-        plan.step([W[0], W[0]], G)            # in-place outputs overlap
+        plan._step_ptrs([W[0], W[0]], G)      # in-place outputs overlap (the C library's check)
     assert e.value.status in (lm.MALT_ERR_ALIAS, lm.MALT_ERR_STATE_MISMATCH)
     with pytest.raises(lm.MaltError) as e:
         plan.step(W, G, lm.make_hparams(mu1=1.0))
@@ -125,3 +127,26 @@ def test_profile_counts_every_launch():
     assert prof["ns_update"]["flops"] == 5 * 2.0 * 2 * 256 * 256 * 512
     again = plan.profile_read()
     assert again["ns_gram"]["launches"] == 0
+
+
+def test_binding_rejects_tensors_the_c_abi_cannot_check():
+    import torch
+    say("[runtime] binding tensor checks")
+    shapes = [(64, 96), (96, 64)]
+    plan = lm.Plan(shapes, "malt")
+    W = to_dev([wl.weight(96, i, s) for i, s in enumerate(shapes)])
+    G = to_dev([wl.grad(96, 1, i, s) for i, s in enumerate(shapes)])
+    bad = [
+        ([W[0].double(), W[1]], G),                      # dtype
+        ([W[0].t().contiguous().t(), W[1]], G),          # non-contiguous (transposed view)
+        (W, [G[0], G[1].reshape(64, 96)]),               # shape
+        ([W[0].cpu(), W[1]], G),                         # device
+    ]
+    for params, grads in bad:
+        with pytest.raises(ValueError):
+            plan.step(params, grads)
+    torch.cuda.synchronize()
+    assert plan.t == 0
+    plan.step(W, G)
+    torch.cuda.synchronize()
+    assert plan.t == 1
