@@ -61,9 +61,10 @@ struct Layout {
   std::vector<MatPlan> mats;
   size_t state_bytes = 0, ws_bytes = 0;
   size_t ws_desc = 0, ws_ptrs = 0;
-  size_t ws_t_ew = 0, ws_t_fin = 0, ws_t_k2 = 0, ws_t_sym = 0, ws_t_upd = 0;
+  size_t ws_t_ew = 0, ws_t_fin = 0, ws_t_k2 = 0, ws_t_gram = 0, ws_t_poly = 0, ws_t_upd = 0;
   size_t ws_t_smg = 0, ws_t_smp = 0, ws_t_smu = 0;
   int64_t n_ew = 0, n_fin = 0, n_k2 = 0, n_sym = 0, n_upd = 0;
+  int64_t n_gram = 0, n_poly = 0, n_updd = 0;   // dispatch-ordered NS lists (padded)
   int64_t n_smg = 0, n_smp = 0, n_smu = 0;   // fp32 Newton-Schulz lists
 };
 
@@ -84,6 +85,97 @@ malt_status_t check_shapes(const malt_shape_t* shapes, int32_t n) {
   }
   return MALT_OK;
 }
+
+// Order of matrices in the grouped work lists: larger Newton-Schulz cost first.
+std::vector<int32_t> cost_order(const Layout& L) {
+  std::vector<int32_t> ord(L.mats.size());
+  for (size_t i = 0; i < ord.size(); ++i) ord[i] = int32_t(i);
+  std::stable_sort(ord.begin(), ord.end(), [&](int32_t a, int32_t b) {
+    return L.mats[a].ns_flops_sym_per_iter > L.mats[b].ns_flops_sym_per_iter;
+  });
+  return ord;
+}
+
+// Newton-Schulz work lists in dispatch order. The cost-ordered list is cut
+// into NXCD contiguous runs of about equal cost (64-k pipeline stages plus a
+// fixed cost per tile), so neighbouring tiles of a matrix, which share operand
+// panels, stay on one XCD while every XCD gets the same work. Workgroup b runs
+// on XCD b % NXCD and takes entry b: the k-th tile of run x sits at
+// NXCD * k + x, and shorter runs are padded with mat = -1.
+std::vector<Tile> xcd_order(const std::vector<Tile>& list, const std::vector<double>& cost) {
+  const size_t n = list.size();
+  if (n == 0) return {};
+  double total = 0.0;
+  for (double c : cost) total += c;
+  size_t off[NXCD + 1];
+  off[0] = 0;
+  double acc = 0.0;
+  size_t i = 0;
+  for (int x = 1; x < NXCD; ++x) {
+    const double target = total * x / NXCD;
+    while (i < n && acc + 0.5 * cost[i] < target) acc += cost[i++];
+    off[x] = i;
+  }
+  off[NXCD] = n;
+  size_t longest = 0;
+  for (int x = 0; x < NXCD; ++x) longest = std::max(longest, off[x + 1] - off[x]);
+  std::vector<Tile> out(NXCD * longest, Tile{-1, 0, 0, 0});
+  for (int x = 0; x < NXCD; ++x)
+    for (size_t k = off[x]; k < off[x + 1]; ++k) out[NXCD * (k - off[x]) + x] = list[k];
+  return out;
+}
+
+// Gram, polynomial and update lists in dispatch order (the Gram and the
+// polynomial share tiles but not costs: K is n' for one and m' for the other).
+void ns_dispatch_lists(const Layout& L, const std::vector<Tile>& sym, const std::vector<Tile>& upd,
+                       std::vector<Tile>& gram, std::vector<Tile>& poly, std::vector<Tile>& upd_d) {
+  constexpr double kTileFixed = 1.5;   // prologue + epilogue, in stages
+  std::vector<double> cg(sym.size()), cp(sym.size()), cu(upd.size());
+  for (size_t k = 0; k < sym.size(); ++k) {
+    const MatPlan& q = L.mats[sym[k].mat];
+    // A diagonal tile loads one operand panel instead of two.
+    const double f = sym[k].ti == sym[k].tj ? 0.75 : 1.0;
+    cg[k] = f * double(q.np) / NS_BK + kTileFixed;
+    cp[k] = f * double(q.mp) / NS_BK + kTileFixed;
+  }
+  for (size_t k = 0; k < upd.size(); ++k) {
+    const MatPlan& q = L.mats[upd[k].mat];
+    cu[k] = double(q.split ? 2 * q.mp : q.mp) / NS_BK + kTileFixed;
+  }
+  gram = xcd_order(sym, cg);
+  poly = xcd_order(sym, cp);
+  upd_d = xcd_order(upd, cu);
+}
+
+void build_tiles(const Layout& L, std::vector<Tile>& ew, std::vector<Tile>& fin, std::vector<Tile>& k2,
+                 std::vector<Tile>& sym, std::vector<Tile>& upd, std::vector<Tile>& smg, std::vector<Tile>& smp,
+                 std::vector<Tile>& smu) {
+  const std::vector<int32_t> ord = cost_order(L);
+  for (int32_t i : ord) {
+    const MatPlan& q = L.mats[i];
+    for (int32_t ti = 0; ti < q.k1_rt; ++ti)
+      for (int32_t tj = 0; tj < q.k1_ct; ++tj) ew.push_back({i, ti, tj, 0});
+    for (int32_t c = 0; c < cdiv(q.m, NTHREADS); ++c) fin.push_back({i, 0, c, 0});
+    for (int32_t c = 0; c < cdiv(q.n, NTHREADS); ++c) fin.push_back({i, 1, c, 0});
+    int32_t idx = 0;
+    for (int32_t ti = 0; ti < q.k2_tr; ++ti)
+      for (int32_t tj = 0; tj < q.k2_tc; ++tj) k2.push_back({i, ti, tj, idx++});
+    if (q.small) {
+      for (int32_t c = 0; c < q.sm_gchunks; ++c) smg.push_back({i, c, 0, 0});
+      smp.push_back({i, 0, 0, 0});
+      for (int32_t c = 0; c < q.upd_tiles; ++c) smu.push_back({i, c, 0, c});
+      continue;
+    }
+    const int32_t T = int32_t(q.mp / NS_TILE), TN = int32_t(q.np / NS_TILE);
+    idx = 0;
+    for (int32_t ti = 0; ti < T; ++ti)
+      for (int32_t tj = ti; tj < T; ++tj) sym.push_back({i, ti, tj, idx++});
+    idx = 0;
+    for (int32_t tj = 0; tj < TN; ++tj)       // column panel major: neighbours share X^T panels
+      for (int32_t ti = 0; ti < T; ++ti) upd.push_back({i, ti, tj, idx++});
+  }
+}
+
 
 Layout make_layout(const malt_shape_t* shapes, int32_t n, malt_variant_t variant) {
   Layout L;
@@ -136,8 +228,18 @@ Layout make_layout(const malt_shape_t* shapes, int32_t n, malt_variant_t variant
   L.ws_t_ew = take(sizeof(Tile) * L.n_ew);
   L.ws_t_fin = take(sizeof(Tile) * L.n_fin);
   L.ws_t_k2 = take(sizeof(Tile) * L.n_k2);
-  L.ws_t_sym = take(sizeof(Tile) * L.n_sym);
-  L.ws_t_upd = take(sizeof(Tile) * L.n_upd);
+  {
+    // The padded lengths of the dispatch-ordered lists depend on the costs.
+    std::vector<Tile> ew, fin, k2, sym, upd, smg, smp, smu, gram, poly, updd;
+    build_tiles(L, ew, fin, k2, sym, upd, smg, smp, smu);
+    ns_dispatch_lists(L, sym, upd, gram, poly, updd);
+    L.n_gram = int64_t(gram.size());
+    L.n_poly = int64_t(poly.size());
+    L.n_updd = int64_t(updd.size());
+  }
+  L.ws_t_gram = take(sizeof(Tile) * L.n_gram);
+  L.ws_t_poly = take(sizeof(Tile) * L.n_poly);
+  L.ws_t_upd = take(sizeof(Tile) * L.n_updd);
   L.ws_t_smg = take(sizeof(Tile) * L.n_smg);
   L.ws_t_smp = take(sizeof(Tile) * L.n_smp);
   L.ws_t_smu = take(sizeof(Tile) * L.n_smu);
@@ -163,16 +265,6 @@ Layout make_layout(const malt_shape_t* shapes, int32_t n, malt_variant_t variant
   }
   L.ws_bytes = off;
   return L;
-}
-
-// Order of matrices in the grouped work lists: larger Newton-Schulz cost first.
-std::vector<int32_t> cost_order(const Layout& L) {
-  std::vector<int32_t> ord(L.mats.size());
-  for (size_t i = 0; i < ord.size(); ++i) ord[i] = int32_t(i);
-  std::stable_sort(ord.begin(), ord.end(), [&](int32_t a, int32_t b) {
-    return L.mats[a].ns_flops_sym_per_iter > L.mats[b].ns_flops_sym_per_iter;
-  });
-  return ord;
 }
 
 bool ranges_overlap(uintptr_t a0, size_t an, uintptr_t b0, size_t bn) {
@@ -286,35 +378,6 @@ void fill_desc(const malt_plan* p, std::vector<MatDesc>& D) {
   }
 }
 
-void build_tiles(const malt_plan* p, std::vector<Tile>& ew, std::vector<Tile>& fin, std::vector<Tile>& k2,
-                 std::vector<Tile>& sym, std::vector<Tile>& upd, std::vector<Tile>& smg, std::vector<Tile>& smp,
-                 std::vector<Tile>& smu) {
-  const std::vector<int32_t> ord = cost_order(p->L);
-  for (int32_t i : ord) {
-    const MatPlan& q = p->L.mats[i];
-    for (int32_t ti = 0; ti < q.k1_rt; ++ti)
-      for (int32_t tj = 0; tj < q.k1_ct; ++tj) ew.push_back({i, ti, tj, 0});
-    for (int32_t c = 0; c < cdiv(q.m, NTHREADS); ++c) fin.push_back({i, 0, c, 0});
-    for (int32_t c = 0; c < cdiv(q.n, NTHREADS); ++c) fin.push_back({i, 1, c, 0});
-    int32_t idx = 0;
-    for (int32_t ti = 0; ti < q.k2_tr; ++ti)
-      for (int32_t tj = 0; tj < q.k2_tc; ++tj) k2.push_back({i, ti, tj, idx++});
-    if (q.small) {
-      for (int32_t c = 0; c < q.sm_gchunks; ++c) smg.push_back({i, c, 0, 0});
-      smp.push_back({i, 0, 0, 0});
-      for (int32_t c = 0; c < q.upd_tiles; ++c) smu.push_back({i, c, 0, c});
-      continue;
-    }
-    const int32_t T = int32_t(q.mp / NS_TILE), TN = int32_t(q.np / NS_TILE);
-    idx = 0;
-    for (int32_t ti = 0; ti < T; ++ti)
-      for (int32_t tj = ti; tj < T; ++tj) sym.push_back({i, ti, tj, idx++});
-    idx = 0;
-    for (int32_t tj = 0; tj < TN; ++tj)       // column panel major: neighbours share X^T panels
-      for (int32_t ti = 0; ti < T; ++ti) upd.push_back({i, ti, tj, idx++});
-  }
-}
-
 }  // namespace
 
 extern "C" {
@@ -382,7 +445,9 @@ malt_status_t malt_init_state(malt_plan_t** out, const malt_shape_t* shapes, int
   std::vector<MatDesc> D;
   fill_desc(p, D);
   std::vector<Tile> ew, fin, k2, sym, upd, smg, smp, smu;
-  build_tiles(p, ew, fin, k2, sym, upd, smg, smp, smu);
+  build_tiles(p->L, ew, fin, k2, sym, upd, smg, smp, smu);
+  std::vector<Tile> gram, poly, updd;
+  ns_dispatch_lists(p->L, sym, upd, gram, poly, updd);
 
   // Stage every table in one pinned buffer laid out like the workspace head.
   const size_t head = p->L.ws_t_smu + sizeof(Tile) * smu.size();
@@ -395,8 +460,9 @@ malt_status_t malt_init_state(malt_plan_t** out, const malt_shape_t* shapes, int
   memcpy(hc + p->L.ws_t_ew, ew.data(), sizeof(Tile) * ew.size());
   memcpy(hc + p->L.ws_t_fin, fin.data(), sizeof(Tile) * fin.size());
   memcpy(hc + p->L.ws_t_k2, k2.data(), sizeof(Tile) * k2.size());
-  memcpy(hc + p->L.ws_t_sym, sym.data(), sizeof(Tile) * sym.size());
-  memcpy(hc + p->L.ws_t_upd, upd.data(), sizeof(Tile) * upd.size());
+  memcpy(hc + p->L.ws_t_gram, gram.data(), sizeof(Tile) * gram.size());
+  memcpy(hc + p->L.ws_t_poly, poly.data(), sizeof(Tile) * poly.size());
+  memcpy(hc + p->L.ws_t_upd, updd.data(), sizeof(Tile) * updd.size());
   memcpy(hc + p->L.ws_t_smg, smg.data(), sizeof(Tile) * smg.size());
   memcpy(hc + p->L.ws_t_smp, smp.data(), sizeof(Tile) * smp.size());
   memcpy(hc + p->L.ws_t_smu, smu.data(), sizeof(Tile) * smu.size());
@@ -529,12 +595,13 @@ malt_status_t malt_step(malt_plan_t* p, float* const* params, const float* const
       na.last = it == hp->ns_steps - 1;
       na.src = it & 1;
       if (p->L.n_sym > 0) {   // matrix-core path
-        na.tiles = tiles_at(p->L.ws_t_sym); na.ntiles = int32_t(p->L.n_sym);
+        na.tiles = tiles_at(p->L.ws_t_gram); na.ntiles = int32_t(p->L.n_gram);
         na.phase = PH_GRAM;
         MALT_LAUNCH(4, launch_ns_gemm(na, s));
+        na.tiles = tiles_at(p->L.ws_t_poly); na.ntiles = int32_t(p->L.n_poly);
         na.phase = PH_POLY;
         MALT_LAUNCH(5, launch_ns_gemm(na, s));
-        na.tiles = tiles_at(p->L.ws_t_upd); na.ntiles = int32_t(p->L.n_upd);
+        na.tiles = tiles_at(p->L.ws_t_upd); na.ntiles = int32_t(p->L.n_updd);
         na.phase = PH_UPDATE;
         MALT_LAUNCH(6, launch_ns_gemm(na, s));
       }

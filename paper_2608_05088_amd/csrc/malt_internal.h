@@ -103,7 +103,8 @@ struct PtrPair {
 //   momentum/back-map: (mat, row tile, col tile, -)
 //   preconditioner finalise: (mat, 0 = rows | 1 = cols, chunk, -)
 //   scale+convert: (mat, row tile, col tile, partial slot)
-//   NS: (mat, tile row, tile col, partial slot)
+//   NS: (mat, tile row, tile col, partial slot), stored in dispatch order:
+//       entry b runs on XCD b % 8; mat = -1 pads the shorter XCD runs
 //   fp32 NS: Gram (mat, chunk, -, -), polynomial (mat, -, -, -),
 //            update (mat, chunk, -, partial slot)
 struct Tile {
@@ -148,6 +149,9 @@ hipError_t launch_graft_scalars(const EwArgs& a, int32_t nmat, hipStream_t s);
 hipError_t launch_backmap_write(const EwArgs& a, hipStream_t s);
 hipError_t launch_ns_gemm(const NsArgs& a, hipStream_t s);
 hipError_t launch_small_ns(const NsArgs& a, hipStream_t s);
+
+// XCDs of the chip; workgroups are dispatched to them round-robin.
+constexpr int NXCD = 8;
 
 // Map a workgroup id to a work index so that the workgroups that land on one
 // XCD (dispatched round-robin over 8 XCDs) take a contiguous run of the work

@@ -271,7 +271,10 @@ void ns_gemm_sym_kernel(NsArgs args) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
   // Every descriptor field the tile needs is read here, before any store, so
   // the uniform loads go through the scalar cache.
-  const Tile t = args.tiles[xcd_remap(blockIdx.x, gridDim.x)];
+  // The work list is in dispatch order (XCD-balanced on the host); entries
+  // with mat < 0 pad the shorter XCD runs.
+  const Tile t = args.tiles[blockIdx.x];
+  if (t.mat < 0) return;
   const MatDesc* __restrict__ d = args.desc + t.mat;
   const int phase = args.phase;
   const int mp = d->mp, np = d->np;
@@ -503,7 +506,10 @@ void ns_update_kernel(NsArgs args) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
   // Every descriptor field the tile needs is read here, before any store, so
   // the uniform loads go through the scalar cache.
-  const Tile t = args.tiles[xcd_remap(blockIdx.x, gridDim.x)];
+  // The work list is in dispatch order (XCD-balanced on the host); entries
+  // with mat < 0 pad the shorter XCD runs.
+  const Tile t = args.tiles[blockIdx.x];
+  if (t.mat < 0) return;
   const MatDesc* __restrict__ d = args.desc + t.mat;
   const int mp = d->mp, np = d->np, mc = d->mc, nc = d->nc;
   const bool tall = d->tall != 0;
