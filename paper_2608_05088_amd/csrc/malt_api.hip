@@ -96,32 +96,63 @@ std::vector<int32_t> cost_order(const Layout& L) {
   return ord;
 }
 
-// Newton-Schulz work lists in dispatch order. The cost-ordered list is cut
-// into NXCD contiguous runs of about equal cost (64-k pipeline stages plus a
-// fixed cost per tile), so neighbouring tiles of a matrix, which share operand
-// panels, stay on one XCD while every XCD gets the same work. Workgroup b runs
-// on XCD b % NXCD and takes entry b: the k-th tile of run x sits at
-// NXCD * k + x, and shorter runs are padded with mat = -1.
+// Newton-Schulz work lists in dispatch order. Workgroup b runs on XCD
+// b % NXCD and takes entry b, so the k-th tile of XCD x's run sits at
+// NXCD * k + x; shorter runs are padded with mat = -1.
+//
+// The runs are filled matrix by matrix, largest first, each matrix going to
+// the run with the least work so far (cost: 64-k pipeline stages per tile plus
+// a fixed cost). Every XCD gets the same work and a mix of shapes, and a
+// matrix's tiles, which share operand panels, stay together in one XCD's L2.
+// A matrix holding more than 1/16 of the launch is first cut into contiguous
+// pieces of at most that size, so a single large matrix still spreads over
+// all XCDs.
 std::vector<Tile> xcd_order(const std::vector<Tile>& list, const std::vector<double>& cost) {
   const size_t n = list.size();
   if (n == 0) return {};
   double total = 0.0;
   for (double c : cost) total += c;
-  size_t off[NXCD + 1];
-  off[0] = 0;
-  double acc = 0.0;
-  size_t i = 0;
-  for (int x = 1; x < NXCD; ++x) {
-    const double target = total * x / NXCD;
-    while (i < n && acc + 0.5 * cost[i] < target) acc += cost[i++];
-    off[x] = i;
+  const double limit = total / (2 * NXCD);
+  struct Item { size_t lo, hi; double c; };
+  std::vector<Item> items;
+  for (size_t lo = 0; lo < n;) {   // the list holds each matrix's tiles contiguously
+    size_t hi = lo;
+    double c = 0.0;
+    while (hi < n && list[hi].mat == list[lo].mat) c += cost[hi++];
+    // Cut [lo, hi) into `pieces` contiguous ranges of about equal cost.
+    const int pieces = std::max(1, int(std::ceil(c / limit)));
+    double acc = 0.0;
+    size_t a = lo;
+    int cut = 1;
+    double pc = 0.0;
+    for (size_t k = lo; k < hi; ++k) {
+      acc += cost[k];
+      pc += cost[k];
+      if (cut < pieces && acc >= c * cut / pieces) {
+        items.push_back({a, k + 1, pc});
+        a = k + 1;
+        pc = 0.0;
+        ++cut;
+      }
+    }
+    if (a < hi) items.push_back({a, hi, pc});
+    lo = hi;
   }
-  off[NXCD] = n;
+  std::stable_sort(items.begin(), items.end(), [](const Item& x, const Item& y) { return x.c > y.c; });
+  std::vector<size_t> runs[NXCD];
+  double load[NXCD] = {0.0};
+  for (const Item& it : items) {
+    int best = 0;
+    for (int x = 1; x < NXCD; ++x)
+      if (load[x] < load[best]) best = x;
+    for (size_t k = it.lo; k < it.hi; ++k) runs[best].push_back(k);
+    load[best] += it.c;
+  }
   size_t longest = 0;
-  for (int x = 0; x < NXCD; ++x) longest = std::max(longest, off[x + 1] - off[x]);
+  for (int x = 0; x < NXCD; ++x) longest = std::max(longest, runs[x].size());
   std::vector<Tile> out(NXCD * longest, Tile{-1, 0, 0, 0});
   for (int x = 0; x < NXCD; ++x)
-    for (size_t k = off[x]; k < off[x + 1]; ++k) out[NXCD * (k - off[x]) + x] = list[k];
+    for (size_t k = 0; k < runs[x].size(); ++k) out[NXCD * k + x] = list[runs[x][k]];
   return out;
 }
 
