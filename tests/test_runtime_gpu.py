@@ -150,3 +150,27 @@ def test_binding_rejects_tensors_the_c_abi_cannot_check():
     plan.step(W, G)
     torch.cuda.synchronize()
     assert plan.t == 1
+
+
+def test_non_finite_gradient_stays_in_its_matrix():
+    """NaN/Inf propagate without checks, but only inside the matrix that has
+    them: every other matrix of the grouped step is bitwise the same as in a
+    step without the bad gradient."""
+    import torch
+    say("[runtime] NaN gradient confined to its matrix")
+    shapes = [(256, 512), (512, 256), (300, 700), (5, 40)]
+    W0 = [wl.weight(95, i, s) for i, s in enumerate(shapes)]
+    G = [wl.grad(95, 1, i, s) for i, s in enumerate(shapes)]
+    bad = [g.copy() for g in G]
+    bad[2][7, 11] = np.nan
+    outs = []
+    for grads in (G, bad):
+        plan = lm.Plan(shapes, "malter")
+        W = to_dev(W0)
+        plan.step(W, to_dev(grads))
+        torch.cuda.synchronize()
+        outs.append([w.cpu().numpy() for w in W])
+        plan.close()
+    for k in (0, 1, 3):
+        assert np.array_equal(outs[0][k], outs[1][k])
+    assert not np.all(np.isfinite(outs[1][2]))
