@@ -26,10 +26,18 @@ __device__ __forceinline__ double wave_sum_d(double v) {
 
 __device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
-// Load 4 consecutive floats of one row starting at column c (columns >= n read 0).
+typedef float ew_f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned ew_u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned ew_u32x4 __attribute__((ext_vector_type(4)));
+
+// Load 4 consecutive floats of one row starting at column c (columns >= n
+// read 0). STREAM marks data this step reads once (non-temporal load).
+template <bool STREAM = false>
 __device__ __forceinline__ void load4(const float* __restrict__ p, int c, int n, bool vec, float v[4]) {
   if (vec && c + 3 < n) {
-    const float4 x = *reinterpret_cast<const float4*>(p + c);
+    ew_f32x4 x;
+    if (STREAM) x = __builtin_nontemporal_load(reinterpret_cast<const ew_f32x4*>(p + c));
+    else x = *reinterpret_cast<const ew_f32x4*>(p + c);
     v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
   } else {
 #pragma unroll
@@ -52,33 +60,41 @@ __device__ __forceinline__ void store4(float* __restrict__ p, int c, int n, bool
 // column sums of G^2 that feed the l, r EMAs (Eq. dp_preconditioner).
 // Reads G and M, writes M: 12 bytes per element.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(NTHREADS) void momentum_rowcol_kernel(EwArgs a) {
-  __shared__ float colsh[4][EW_TC];
+__global__ __launch_bounds__(EW_THREADS) void momentum_rowcol_kernel(EwArgs a) {
+  constexpr int NW = EW_THREADS / 64, RPW = EW_TR / NW;   // 16 waves, 2 rows each
+  static_assert(NW * RPW == EW_TR && EW_TC == 256, "one 256-column row segment per wave and row");
+  __shared__ float colsh[NW][EW_TC];
   const Tile t = a.tiles[xcd_remap(blockIdx.x, gridDim.x)];
   const MatDesc& d = a.desc[t.mat];
   const int m = d.m, n = d.n;
   const bool vec = a.ptrs[t.mat].vec != 0;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int r0 = t.ti * EW_TR, c = t.tj * EW_TC + lane * 4;
+  const int r0 = t.ti * EW_TR + w * RPW, c = t.tj * EW_TC + lane * 4;
   const float* __restrict__ G = a.ptrs[t.mat].G;
   float* __restrict__ M = d.M;
+  float g[RPW][4], mm[RPW][4];
+#pragma unroll
+  for (int u = 0; u < RPW; ++u) {
+    if (r0 + u < m) {
+      const size_t off = (size_t)(r0 + u) * n;
+      load4<true>(G + off, c, n, vec, g[u]);
+      load4(M + off, c, n, vec, mm[u]);
+    }
+  }
   float cacc[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int rr = w; rr < EW_TR; rr += 4) {
-    const int r = r0 + rr;
-    if (r >= m) break;
-    const size_t off = (size_t)r * n;
-    float g[4], mm[4];
-    load4(G + off, c, n, vec, g);
-    load4(M + off, c, n, vec, mm);
+#pragma unroll
+  for (int u = 0; u < RPW; ++u) {
+    const int r = r0 + u;
+    if (r >= m) break;   // uniform over the wave
     float racc = 0.f;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      mm[e] = a.mu1 * mm[e] + a.one_minus_mu1 * g[e];
-      const float g2 = g[e] * g[e];
+      mm[u][e] = a.mu1 * mm[u][e] + a.one_minus_mu1 * g[u][e];
+      const float g2 = g[u][e] * g[u][e];
       racc += g2;
       cacc[e] += g2;
     }
-    store4(M + off, c, n, vec, mm);
+    store4(M + (size_t)r * n, c, n, vec, mm[u]);
     racc = wave_sum(racc);
     if (lane == 0) d.rowpart[(size_t)t.tj * m + r] = racc;
   }
@@ -87,8 +103,10 @@ __global__ __launch_bounds__(NTHREADS) void momentum_rowcol_kernel(EwArgs a) {
   __syncthreads();
   const int cc = threadIdx.x;
   const int col = t.tj * EW_TC + cc;
-  if (col < n) {
-    const float s = (colsh[0][cc] + colsh[1][cc]) + (colsh[2][cc] + colsh[3][cc]);
+  if (cc < EW_TC && col < n) {
+    float s = 0.f;
+#pragma unroll
+    for (int k = 0; k < NW; ++k) s += colsh[k][cc];
     d.colpart[(size_t)t.ti * n + col] = s;
   }
 }
@@ -118,19 +136,88 @@ __global__ __launch_bounds__(NTHREADS) void precond_finalize_kernel(EwArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// X0 = bf16(L M R) in the canonical orientation (W for wide matrices, W^T
-// through an LDS transpose for tall ones) over the zero-padded domain, plus
-// per-tile sums of (LMR)^2 and, for MALTER, (LGR)^2.  Tiles cover W-oriented
-// padded rows x cols in K2_T x K2_T blocks, K2_GROUP tiles per workgroup.
+// X0 = bf16(L M R) in the canonical orientation over the zero-padded domain,
+// plus per-tile sums of (LMR)^2 and, for MALTER, (LGR)^2.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(NTHREADS) void scale_convert_kernel(EwArgs a) {
-  // One workgroup converts K2_GROUP consecutive tiles: a 64-row band of
-  // K2_GROUP * 64 W columns of one matrix (a matrix's tiles are listed band by
-  // band, and every band holds a multiple of K2_GROUP tiles).  All loads of the
-  // band are issued before any conversion.
+// Wide matrices: the canonical matrix is W. Tiles of K2W_R padded rows x
+// EW_TC padded columns; each wave converts K2W_R / waves consecutive rows, one
+// float4 of M (and of G) per lane and row, all loads issued first.
+template <bool MALTER>
+__global__ __launch_bounds__(K2W_THREADS) void scale_convert_wide_kernel(EwArgs a) {
+  constexpr int NW = K2W_THREADS / 64, RPW = K2W_R / NW;
+  static_assert(NW * RPW == K2W_R && EW_TC == 256, "whole 256-column row segments per wave");
+  __shared__ float red[2][NW];
+  const Tile t = a.tiles[xcd_remap(blockIdx.x, gridDim.x)];
+  const MatDesc& d = a.desc[t.mat];
+  const int m = d.m, n = d.n;
+  const bool vec = a.ptrs[t.mat].vec != 0;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int rw = t.ti * K2W_R + w * RPW, c = t.tj * EW_TC + lane * 4;   // rows < mp, c < np
+  float mm[RPW][4], gg[RPW][4], rv[4];
+#pragma unroll
+  for (int u = 0; u < RPW; ++u) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) mm[u][e] = gg[u][e] = 0.f;
+    if (rw + u < m) {
+      load4(d.M + (size_t)(rw + u) * n, c, n, vec, mm[u]);
+      if (MALTER) load4(a.ptrs[t.mat].G + (size_t)(rw + u) * n, c, n, vec, gg[u]);
+    }
+  }
+  load4(d.Rv, c, n, true, rv);
+  float s2 = 0.f, q2 = 0.f;
+#pragma unroll
+  for (int u = 0; u < RPW; ++u) {
+    const int r = rw + u;
+    const float li = r < m ? d.Lv[r] : 0.f;
+    float x[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[e] = li * mm[u][e] * rv[e];
+      s2 += x[e] * x[e];
+      if (MALTER) {
+        const float y = li * gg[u][e] * rv[e];
+        q2 += y * y;
+      }
+    }
+    // X0 is consumed by the next kernel from L2/HBM; streaming store.
+    const ew_u32x2 pk = {pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3])};
+    __builtin_nontemporal_store(pk, reinterpret_cast<ew_u32x2*>(d.X[0] + (size_t)r * d.np + c));
+  }
+  s2 = wave_sum(s2);
+  if (MALTER) q2 = wave_sum(q2);
+  if (lane == 0) {
+    red[0][w] = s2;
+    red[1][w] = q2;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float so = 0.f, sq = 0.f;
+#pragma unroll
+    for (int k = 0; k < NW; ++k) {
+      so += red[0][k];
+      sq += red[1][k];
+    }
+    d.k2part[2 * (size_t)t.idx + 0] = so;
+    d.k2part[2 * (size_t)t.idx + 1] = sq;
+  }
+}
+
+// Tall matrices: the canonical matrix is W^T, written through an LDS
+// transpose. Tiles cover W-oriented padded rows x cols in K2_T x K2_T blocks;
+// one workgroup converts K2_GROUP consecutive tiles, a 64-row band of
+// K2_GROUP * 64 W columns of one matrix (a matrix's tiles are listed band by
+// band, and every band holds a multiple of K2_GROUP tiles). All loads of the
+// band are issued before any conversion.
+template <bool MALTER>
+__global__ __launch_bounds__(K2T_THREADS) void scale_convert_tall_kernel(EwArgs a) {
   constexpr int TG = K2_GROUP;
+  constexpr int NW = K2T_THREADS / 64;
+  constexpr int RQ = K2T_THREADS / 16;   // row groups: 16 threads x 4 columns span a tile's 64 columns
+  constexpr int P = K2_T / RQ;           // rows per thread and tile
+  constexpr int SEGS = K2T_THREADS / K2_T, SEG = K2_T / SEGS;   // transposed write: W rows per thread
+  static_assert(P * RQ == K2_T && SEGS * SEG == K2_T && SEG % 8 == 0, "tall tile layout");
   __shared__ bf16_t tsh[TG][K2_T][K2_T + 2];
-  __shared__ float red[2 * TG][4];
+  __shared__ float red[2 * TG][NW];
   const int grp = xcd_remap(blockIdx.x, gridDim.x);
   const Tile t = a.tiles[grp * TG];
   const MatDesc& d = a.desc[t.mat];
@@ -140,15 +227,14 @@ __global__ __launch_bounds__(NTHREADS) void scale_convert_kernel(EwArgs a) {
   const int ldx = d.np;                  // canonical row pitch
   const float* __restrict__ M = d.M;
   const float* __restrict__ G = a.ptrs[t.mat].G;
-  const bool malter = a.malter != 0;
   const int r0 = t.ti * K2_T, cb = t.tj * K2_T;   // band columns cb .. cb + TG*K2_T
   const int cc = (threadIdx.x & 15) * 4;          // 4 columns of each tile
-  const int rq = threadIdx.x >> 4;                // rows rq + 16p, p = 0..3
+  const int rq = threadIdx.x >> 4;                // rows rq + RQ p, p < P
 
-  float Li[4];
+  float Li[P];
 #pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    const int r = r0 + p * 16 + rq;
+  for (int p = 0; p < P; ++p) {
+    const int r = r0 + p * RQ + rq;
     Li[p] = r < m ? d.Lv[r] : 0.f;
   }
   float Rv[TG][4];
@@ -159,18 +245,18 @@ __global__ __launch_bounds__(NTHREADS) void scale_convert_kernel(EwArgs a) {
       const int c = cb + j * K2_T + cc + e;
       Rv[j][e] = c < n ? d.Rv[c] : 0.f;
     }
-  float mm[TG][4][4], gg[TG][4][4];
+  float mm[TG][P][4], gg[TG][P][4];
 #pragma unroll
   for (int j = 0; j < TG; ++j)
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      const int r = r0 + p * 16 + rq;
+    for (int p = 0; p < P; ++p) {
+      const int r = r0 + p * RQ + rq;
       const int c = cb + j * K2_T + cc;
 #pragma unroll
       for (int e = 0; e < 4; ++e) mm[j][p][e] = gg[j][p][e] = 0.f;
       if (r < m) {
         load4(M + (size_t)r * n, c, n, vec, mm[j][p]);
-        if (malter) load4(G + (size_t)r * n, c, n, vec, gg[j][p]);
+        if (MALTER) load4(G + (size_t)r * n, c, n, vec, gg[j][p]);
       }
     }
 
@@ -179,52 +265,50 @@ __global__ __launch_bounds__(NTHREADS) void scale_convert_kernel(EwArgs a) {
   for (int j = 0; j < TG; ++j) {
     s2[j] = 0.f;
     q2[j] = 0.f;
-    const int c0 = cb + j * K2_T;
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      const int rr = p * 16 + rq;
+    for (int p = 0; p < P; ++p) {
+      const int rr = p * RQ + rq;
       float x[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         x[e] = Li[p] * mm[j][p][e] * Rv[j][e];
         s2[j] += x[e] * x[e];
-        const float y = Li[p] * gg[j][p][e] * Rv[j][e];   // zero for MALT (gg = 0)
-        q2[j] += y * y;
+        if (MALTER) {
+          const float y = Li[p] * gg[j][p][e] * Rv[j][e];
+          q2[j] += y * y;
+        }
       }
-      uint2 pk;
-      pk.x = pack_bf16x2(x[0], x[1]);
-      pk.y = pack_bf16x2(x[2], x[3]);
-      if (!d.tall) {
-        *reinterpret_cast<uint2*>(X0 + (size_t)(r0 + rr) * ldx + c0 + cc) = pk;
-      } else {
-        tsh[j][rr][cc + 0] = (bf16_t)(pk.x & 0xffffu);
-        tsh[j][rr][cc + 1] = (bf16_t)(pk.x >> 16);
-        tsh[j][rr][cc + 2] = (bf16_t)(pk.y & 0xffffu);
-        tsh[j][rr][cc + 3] = (bf16_t)(pk.y >> 16);
-      }
+      const uint32_t lo = pack_bf16x2(x[0], x[1]), hi = pack_bf16x2(x[2], x[3]);
+      tsh[j][rr][cc + 0] = (bf16_t)(lo & 0xffffu);
+      tsh[j][rr][cc + 1] = (bf16_t)(lo >> 16);
+      tsh[j][rr][cc + 2] = (bf16_t)(hi & 0xffffu);
+      tsh[j][rr][cc + 3] = (bf16_t)(hi >> 16);
     }
   }
-  if (d.tall) {
-    __syncthreads();
-    // Transposed write: thread -> (W column ct, 16-row segment) of each tile.
-    const int ct = threadIdx.x >> 2;
-    const int seg = (threadIdx.x & 3) * 16;
+  __syncthreads();
+  // Transposed write: thread -> (W column ct, SEG-row segment) of each tile.
+  const int ct = threadIdx.x / SEGS;
+  const int seg = (threadIdx.x % SEGS) * SEG;
 #pragma unroll
-    for (int j = 0; j < TG; ++j) {
-      uint32_t wv[8];
+  for (int j = 0; j < TG; ++j) {
+    ew_u32x4* dst = reinterpret_cast<ew_u32x4*>(X0 + (size_t)(cb + j * K2_T + ct) * ldx + r0 + seg);
 #pragma unroll
-      for (int k = 0; k < 8; ++k)
-        wv[k] = (uint32_t)tsh[j][seg + 2 * k][ct] | ((uint32_t)tsh[j][seg + 2 * k + 1][ct] << 16);
-      uint4* dst = reinterpret_cast<uint4*>(X0 + (size_t)(cb + j * K2_T + ct) * ldx + r0 + seg);
-      dst[0] = make_uint4(wv[0], wv[1], wv[2], wv[3]);
-      dst[1] = make_uint4(wv[4], wv[5], wv[6], wv[7]);
+    for (int h = 0; h < SEG / 8; ++h) {
+      uint32_t wv[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int rr = seg + 8 * h + 2 * k;
+        wv[k] = (uint32_t)tsh[j][rr][ct] | ((uint32_t)tsh[j][rr + 1][ct] << 16);
+      }
+      const ew_u32x4 v = {wv[0], wv[1], wv[2], wv[3]};
+      __builtin_nontemporal_store(v, dst + h);
     }
   }
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
 #pragma unroll
   for (int j = 0; j < TG; ++j) {
     const float sj = wave_sum(s2[j]);
-    const float qj = wave_sum(q2[j]);
+    const float qj = MALTER ? wave_sum(q2[j]) : 0.f;
     if (lane == 0) {
       red[2 * j][w] = sj;
       red[2 * j + 1][w] = qj;
@@ -233,9 +317,14 @@ __global__ __launch_bounds__(NTHREADS) void scale_convert_kernel(EwArgs a) {
   __syncthreads();
   if (threadIdx.x < TG) {
     const int j = threadIdx.x;
-    d.k2part[2 * (size_t)(t.idx + j) + 0] = (red[2 * j][0] + red[2 * j][1]) + (red[2 * j][2] + red[2 * j][3]);
-    d.k2part[2 * (size_t)(t.idx + j) + 1] =
-        (red[2 * j + 1][0] + red[2 * j + 1][1]) + (red[2 * j + 1][2] + red[2 * j + 1][3]);
+    float so = 0.f, sq = 0.f;
+#pragma unroll
+    for (int k = 0; k < NW; ++k) {
+      so += red[2 * j][k];
+      sq += red[2 * j + 1][k];
+    }
+    d.k2part[2 * (size_t)(t.idx + j) + 0] = so;
+    d.k2part[2 * (size_t)(t.idx + j) + 1] = sq;
   }
 }
 
@@ -302,7 +391,9 @@ __global__ __launch_bounds__(NTHREADS) void graft_scalars_kernel(EwArgs a) {
 // W^T for tall ones (read through an LDS transpose).  Reads W and O, writes
 // W: 10 bytes per element.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(NTHREADS) void backmap_write_kernel(EwArgs a) {
+__global__ __launch_bounds__(EW_THREADS) void backmap_write_kernel(EwArgs a) {
+  constexpr int NW = EW_THREADS / 64, RPW = EW_TR / NW;   // 16 waves, 2 rows each
+  static_assert(NW * RPW == EW_TR && EW_TC * EW_TR == EW_THREADS * 8, "tall fill: 8 bf16 per thread");
   __shared__ bf16_t osh[EW_TC][EW_TR + 2];   // tall: O^T block, [W col][W row]
   const Tile t = a.tiles[xcd_remap(blockIdx.x, gridDim.x)];
   const MatDesc& d = a.desc[t.mat];
@@ -317,49 +408,57 @@ __global__ __launch_bounds__(NTHREADS) void backmap_write_kernel(EwArgs a) {
   const float decay = a.decay;
   if (d.tall) {
     // Canonical rows c0 .. c0+255 (W columns), columns r0 .. r0+31 (W rows):
-    // one 64-byte row segment per thread (inside the padded buffer).
-    const uint4* srow = reinterpret_cast<const uint4*>(O + (size_t)(c0 + threadIdx.x) * ldo + r0);
+    // four threads per canonical row, 16 bytes each (inside the padded buffer).
+    const int cr = threadIdx.x >> 2, q = threadIdx.x & 3;
+    const ew_u32x4 v =
+        __builtin_nontemporal_load(reinterpret_cast<const ew_u32x4*>(O + (size_t)(c0 + cr) * ldo + r0 + q * 8));
+    const uint32_t vw[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint4 v = srow[q];
-      const uint32_t vw[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        osh[threadIdx.x][q * 8 + 2 * k] = (bf16_t)(vw[k] & 0xffffu);
-        osh[threadIdx.x][q * 8 + 2 * k + 1] = (bf16_t)(vw[k] >> 16);
-      }
+    for (int k = 0; k < 4; ++k) {
+      osh[cr][q * 8 + 2 * k] = (bf16_t)(vw[k] & 0xffffu);
+      osh[cr][q * 8 + 2 * k + 1] = (bf16_t)(vw[k] >> 16);
     }
     __syncthreads();
   }
   float Rv[4];
+  load4(d.Rv, c, n, true, Rv);
+  const int rw = r0 + w * RPW;   // this wave's first row
+  float wv[RPW][4];
+  uint2 pk[RPW];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) Rv[e] = (c + e < n) ? d.Rv[c + e] : 0.f;
-  for (int rr = w; rr < EW_TR; rr += 4) {
-    const int r = r0 + rr;
-    if (r >= m) break;
+  for (int u = 0; u < RPW; ++u) {
+    if (rw + u < m) {
+      load4(W + (size_t)(rw + u) * n, c, n, vec, wv[u]);
+      if (!d.tall) {
+        const ew_u32x2 q = __builtin_nontemporal_load(reinterpret_cast<const ew_u32x2*>(O + (size_t)(rw + u) * ldo + c));
+        pk[u] = make_uint2(q.x, q.y);
+      }
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < RPW; ++u) {
+    const int r = rw + u;
+    if (r >= m) break;   // uniform over the wave
     const float cl = coef * d.Lv[r];
-    float wv[4];
-    load4(W + (size_t)r * n, c, n, vec, wv);
     float o[4];
     if (!d.tall) {
-      const uint2 pk = *reinterpret_cast<const uint2*>(O + (size_t)r * ldo + c);
-      o[0] = bf2f((bf16_t)(pk.x & 0xffffu));
-      o[1] = bf2f((bf16_t)(pk.x >> 16));
-      o[2] = bf2f((bf16_t)(pk.y & 0xffffu));
-      o[3] = bf2f((bf16_t)(pk.y >> 16));
+      o[0] = bf2f((bf16_t)(pk[u].x & 0xffffu));
+      o[1] = bf2f((bf16_t)(pk[u].x >> 16));
+      o[2] = bf2f((bf16_t)(pk[u].y & 0xffffu));
+      o[3] = bf2f((bf16_t)(pk[u].y >> 16));
     } else {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) o[e] = bf2f(osh[lane * 4 + e][rr]);
+      for (int e = 0; e < 4; ++e) o[e] = bf2f(osh[lane * 4 + e][w * RPW + u]);
     }
 #pragma unroll
-    for (int e = 0; e < 4; ++e) wv[e] = decay * wv[e] - cl * o[e] * Rv[e];
-    store4(W + (size_t)r * n, c, n, vec, wv);
+    for (int e = 0; e < 4; ++e) wv[u][e] = decay * wv[u][e] - cl * o[e] * Rv[e];
+    store4(W + (size_t)r * n, c, n, vec, wv[u]);
   }
 }
 
 hipError_t launch_momentum_rowcol(const EwArgs& a, hipStream_t s) {
   if (a.ntiles == 0) return hipSuccess;
-  hipLaunchKernelGGL(momentum_rowcol_kernel, dim3(a.ntiles), dim3(NTHREADS), 0, s, a);
+  hipLaunchKernelGGL(momentum_rowcol_kernel, dim3(a.ntiles), dim3(EW_THREADS), 0, s, a);
   return hipGetLastError();
 }
 hipError_t launch_precond_finalize(const EwArgs& a, hipStream_t s) {
@@ -367,10 +466,17 @@ hipError_t launch_precond_finalize(const EwArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(precond_finalize_kernel, dim3(a.ntiles), dim3(NTHREADS), 0, s, a);
   return hipGetLastError();
 }
-hipError_t launch_scale_convert(const EwArgs& a, hipStream_t s) {
+hipError_t launch_scale_convert(const EwArgs& a, bool tall, hipStream_t s) {
   if (a.ntiles == 0) return hipSuccess;
+  if (!tall) {
+    if (a.malter) hipLaunchKernelGGL(scale_convert_wide_kernel<true>, dim3(a.ntiles), dim3(K2W_THREADS), 0, s, a);
+    else hipLaunchKernelGGL(scale_convert_wide_kernel<false>, dim3(a.ntiles), dim3(K2W_THREADS), 0, s, a);
+    return hipGetLastError();
+  }
   if (a.ntiles % K2_GROUP != 0) return hipErrorInvalidValue;   // bands hold whole groups
-  hipLaunchKernelGGL(scale_convert_kernel, dim3(a.ntiles / K2_GROUP), dim3(NTHREADS), 0, s, a);
+  const dim3 grid(a.ntiles / K2_GROUP);
+  if (a.malter) hipLaunchKernelGGL(scale_convert_tall_kernel<true>, grid, dim3(K2T_THREADS), 0, s, a);
+  else hipLaunchKernelGGL(scale_convert_tall_kernel<false>, grid, dim3(K2T_THREADS), 0, s, a);
   return hipGetLastError();
 }
 hipError_t launch_norm_scalars(const EwArgs& a, int32_t nmat, hipStream_t s) {
@@ -385,7 +491,7 @@ hipError_t launch_graft_scalars(const EwArgs& a, int32_t nmat, hipStream_t s) {
 }
 hipError_t launch_backmap_write(const EwArgs& a, hipStream_t s) {
   if (a.ntiles == 0) return hipSuccess;
-  hipLaunchKernelGGL(backmap_write_kernel, dim3(a.ntiles), dim3(NTHREADS), 0, s, a);
+  hipLaunchKernelGGL(backmap_write_kernel, dim3(a.ntiles), dim3(EW_THREADS), 0, s, a);
   return hipGetLastError();
 }
 

@@ -64,6 +64,7 @@ struct Layout {
   size_t ws_t_ew = 0, ws_t_fin = 0, ws_t_k2 = 0, ws_t_gram = 0, ws_t_poly = 0, ws_t_upd = 0;
   size_t ws_t_smg = 0, ws_t_smp = 0, ws_t_smu = 0;
   int64_t n_ew = 0, n_fin = 0, n_k2 = 0, n_sym = 0, n_upd = 0;
+  int64_t n_k2w = 0;   // scale+convert tiles of wide matrices, listed before those of tall ones
   int64_t n_gram = 0, n_poly = 0, n_updd = 0;   // dispatch-ordered NS lists (padded)
   int64_t n_smg = 0, n_smp = 0, n_smu = 0;   // fp32 Newton-Schulz lists
 };
@@ -188,9 +189,6 @@ void build_tiles(const Layout& L, std::vector<Tile>& ew, std::vector<Tile>& fin,
       for (int32_t tj = 0; tj < q.k1_ct; ++tj) ew.push_back({i, ti, tj, 0});
     for (int32_t c = 0; c < cdiv(q.m, NTHREADS); ++c) fin.push_back({i, 0, c, 0});
     for (int32_t c = 0; c < cdiv(q.n, NTHREADS); ++c) fin.push_back({i, 1, c, 0});
-    int32_t idx = 0;
-    for (int32_t ti = 0; ti < q.k2_tr; ++ti)
-      for (int32_t tj = 0; tj < q.k2_tc; ++tj) k2.push_back({i, ti, tj, idx++});
     if (q.small) {
       for (int32_t c = 0; c < q.sm_gchunks; ++c) smg.push_back({i, c, 0, 0});
       smp.push_back({i, 0, 0, 0});
@@ -198,13 +196,22 @@ void build_tiles(const Layout& L, std::vector<Tile>& ew, std::vector<Tile>& fin,
       continue;
     }
     const int32_t T = int32_t(q.mp / NS_TILE), TN = int32_t(q.np / NS_TILE);
-    idx = 0;
+    int32_t idx = 0;
     for (int32_t ti = 0; ti < T; ++ti)
       for (int32_t tj = ti; tj < T; ++tj) sym.push_back({i, ti, tj, idx++});
     idx = 0;
     for (int32_t tj = 0; tj < TN; ++tj)       // column panel major: neighbours share X^T panels
       for (int32_t ti = 0; ti < T; ++ti) upd.push_back({i, ti, tj, idx++});
   }
+  // Scale+convert: the wide matrices' tiles, then the tall ones' (two kernels).
+  for (int pass = 0; pass < 2; ++pass)
+    for (int32_t i : ord) {
+      const MatPlan& q = L.mats[i];
+      if (q.tall != (pass == 1)) continue;
+      int32_t idx = 0;
+      for (int32_t ti = 0; ti < q.k2_tr; ++ti)
+        for (int32_t tj = 0; tj < q.k2_tc; ++tj) k2.push_back({i, ti, tj, idx++});
+    }
 }
 
 
@@ -231,8 +238,9 @@ Layout make_layout(const malt_shape_t* shapes, int32_t n, malt_variant_t variant
     p.split = !p.small && p.mc <= NS_SPLIT_MAX;
     p.sm_gchunks = p.small ? cdiv(p.np, SM_CH_G) : 0;
     p.k1_ct = cdiv(p.n, EW_TC); p.k1_rt = cdiv(p.m, EW_TR);
-    const int64_t wrows_p = p.tall ? p.np : p.mp, wcols_p = p.tall ? p.mp : p.np;
-    p.k2_tr = wrows_p / K2_T; p.k2_tc = wcols_p / K2_T;
+    // Scale+convert tiles over the padded W-oriented domain.
+    if (p.tall) { p.k2_tr = p.np / K2_T; p.k2_tc = p.mp / K2_T; }
+    else { p.k2_tr = p.mp / K2W_R; p.k2_tc = p.np / EW_TC; }
     p.k2_tiles = p.k2_tr * p.k2_tc;
     const int64_t T = p.mp / NS_TILE;
     // fp32 path: no matrix-core tiles; the update's partial slots are its
@@ -243,6 +251,7 @@ Layout make_layout(const malt_shape_t* shapes, int32_t n, malt_variant_t variant
     L.n_ew += p.k1_rt * p.k1_ct;
     L.n_fin += cdiv(p.m, NTHREADS) + cdiv(p.n, NTHREADS);
     L.n_k2 += p.k2_tiles;
+    if (!p.tall) L.n_k2w += p.k2_tiles;
     if (p.small) {
       L.n_smg += p.sm_gchunks;
       L.n_smp += 1;
@@ -615,8 +624,14 @@ malt_status_t malt_step(malt_plan_t* p, float* const* params, const float* const
     MALT_LAUNCH(0, launch_momentum_rowcol(ea, s));
     ea.tiles = tiles_at(p->L.ws_t_fin); ea.ntiles = int32_t(p->L.n_fin);
     MALT_LAUNCH(1, launch_precond_finalize(ea, s));
-    ea.tiles = tiles_at(p->L.ws_t_k2); ea.ntiles = int32_t(p->L.n_k2);
-    MALT_LAUNCH(2, launch_scale_convert(ea, s));
+    if (p->L.n_k2w > 0) {
+      ea.tiles = tiles_at(p->L.ws_t_k2); ea.ntiles = int32_t(p->L.n_k2w);
+      MALT_LAUNCH(2, launch_scale_convert(ea, false, s));
+    }
+    if (p->L.n_k2 > p->L.n_k2w) {
+      ea.tiles = tiles_at(p->L.ws_t_k2) + p->L.n_k2w; ea.ntiles = int32_t(p->L.n_k2 - p->L.n_k2w);
+      MALT_LAUNCH(2, launch_scale_convert(ea, true, s));
+    }
     MALT_LAUNCH(3, launch_norm_scalars(ea, n, s));
     NsArgs na;
     na.desc = ea.desc;

@@ -7,14 +7,24 @@
 namespace malt {
 
 // Elementwise tiles (momentum / back-map): EW_TR rows x EW_TC cols per
-// 256-thread workgroup; each lane owns 4 consecutive columns.
+// EW_THREADS-thread workgroup; each lane owns 4 consecutive columns and each
+// wave EW_TR / 16 = 2 rows, whose loads it issues before any arithmetic.
+// (A streaming pass runs closest to HBM's rate with few loads in flight per
+// wave and no loop per wave.)
 constexpr int EW_TR = 32;
 constexpr int EW_TC = 256;
-// Scale+convert tile (with an LDS transpose): K2_T x K2_T; a workgroup takes
-// K2_GROUP consecutive tiles of one row band (padded W dimensions are
-// multiples of 256 = K2_GROUP * K2_T, so bands hold whole groups).
+constexpr int EW_THREADS = 1024;
+// Scale+convert of wide matrices (canonical = W): K2W_R rows x EW_TC cols per
+// K2W_THREADS-thread workgroup, one float4 per lane and row.
+constexpr int K2W_R = 16;
+constexpr int K2W_THREADS = 256;
+// Scale+convert of tall matrices (canonical = W^T, through an LDS transpose):
+// K2_T x K2_T tiles; a K2T_THREADS-thread workgroup takes K2_GROUP consecutive
+// tiles of one row band (padded W dimensions are multiples of 256, so bands
+// hold whole groups).
 constexpr int K2_T = 64;
-constexpr int K2_GROUP = 4;
+constexpr int K2_GROUP = 2;
+constexpr int K2T_THREADS = 512;
 // Newton-Schulz output tile and padding unit of the bf16 buffers.
 constexpr int NS_TILE = 256;
 constexpr int NS_BK = 64;
@@ -143,7 +153,7 @@ struct NsArgs {
 // Launchers (stream-ordered, no synchronisation).
 hipError_t launch_momentum_rowcol(const EwArgs& a, hipStream_t s);
 hipError_t launch_precond_finalize(const EwArgs& a, hipStream_t s);
-hipError_t launch_scale_convert(const EwArgs& a, hipStream_t s);
+hipError_t launch_scale_convert(const EwArgs& a, bool tall, hipStream_t s);
 hipError_t launch_norm_scalars(const EwArgs& a, int32_t nmat, hipStream_t s);
 hipError_t launch_graft_scalars(const EwArgs& a, int32_t nmat, hipStream_t s);
 hipError_t launch_backmap_write(const EwArgs& a, hipStream_t s);
