@@ -194,15 +194,18 @@ def _bf16_rne(x32):
     return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
 
 
-def test_scale_convert_is_bitexact_rne():
+@pytest.mark.parametrize("variant", ["malt", "malter"])
+def test_scale_convert_is_bitexact_rne(variant):
     # X0 = bf16((L_i * M_ij) * R_j) in float32, exactly as a host RNE of the same
-    # float32 product of the GPU's own L, M, R (byte-exact work).
+    # float32 product of the GPU's own L, M, R (byte-exact work). Wide and tall
+    # matrices take different kernels; rows of 47 and 201 floats are not
+    # 16-byte multiples (scalar tails).
     import torch
-    shapes = [(200, 520), (520, 200), (33, 47)]
-    say(f"[parity] bf16 conversion bit-exact {shapes}")
+    shapes = [(200, 520), (520, 200), (33, 47), (300, 201), (201, 300)]
+    say(f"[parity] bf16 conversion bit-exact {variant} {shapes}")
     W0 = [wl.weight(99, i, s) for i, s in enumerate(shapes)]
     G = [wl.grad(99, 1, i, s, "student_t3") for i, s in enumerate(shapes)]
-    plan = lm.Plan(shapes, "malt")
+    plan = lm.Plan(shapes, variant)
     Wd, Gd = to_dev(W0), to_dev(G)
     plan.step(Wd, Gd, lm.make_hparams(lr=1e-2, ns_steps=1))
     torch.cuda.synchronize()
