@@ -33,11 +33,11 @@ typedef unsigned ew_u32x4 __attribute__((ext_vector_type(4)));
 // Load 4 consecutive floats of one row starting at column c (columns >= n
 // read 0). STREAM marks data this step reads once (non-temporal load).
 template <bool STREAM = false>
-__device__ __forceinline__ void load4(const float* __restrict__ p, int c, int n, bool vec, float v[4]) {
+__device__ __forceinline__ void load4(const MALT_GLOBAL float* __restrict__ p, int c, int n, bool vec, float v[4]) {
   if (vec && c + 3 < n) {
     ew_f32x4 x;
-    if (STREAM) x = __builtin_nontemporal_load(reinterpret_cast<const ew_f32x4*>(p + c));
-    else x = *reinterpret_cast<const ew_f32x4*>(p + c);
+    if (STREAM) x = __builtin_nontemporal_load(reinterpret_cast<const MALT_GLOBAL ew_f32x4*>(p + c));
+    else x = *reinterpret_cast<const MALT_GLOBAL ew_f32x4*>(p + c);
     v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
   } else {
 #pragma unroll
@@ -45,9 +45,10 @@ __device__ __forceinline__ void load4(const float* __restrict__ p, int c, int n,
   }
 }
 
-__device__ __forceinline__ void store4(float* __restrict__ p, int c, int n, bool vec, const float v[4]) {
+__device__ __forceinline__ void store4(MALT_GLOBAL float* __restrict__ p, int c, int n, bool vec, const float v[4]) {
   if (vec && c + 3 < n) {
-    *reinterpret_cast<float4*>(p + c) = make_float4(v[0], v[1], v[2], v[3]);
+    const ew_f32x4 x = {v[0], v[1], v[2], v[3]};
+    *reinterpret_cast<MALT_GLOBAL ew_f32x4*>(p + c) = x;
   } else {
 #pragma unroll
     for (int e = 0; e < 4; ++e)
@@ -70,8 +71,8 @@ __global__ __launch_bounds__(EW_THREADS) void momentum_rowcol_kernel(EwArgs a) {
   const bool vec = a.ptrs[t.mat].vec != 0;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int r0 = t.ti * EW_TR + w * RPW, c = t.tj * EW_TC + lane * 4;
-  const float* __restrict__ G = a.ptrs[t.mat].G;
-  float* __restrict__ M = d.M;
+  const MALT_GLOBAL float* __restrict__ G = gptr(a.ptrs[t.mat].G);
+  MALT_GLOBAL float* __restrict__ M = gptr(d.M);
   float g[RPW][4], mm[RPW][4];
 #pragma unroll
   for (int u = 0; u < RPW; ++u) {
@@ -96,7 +97,7 @@ __global__ __launch_bounds__(EW_THREADS) void momentum_rowcol_kernel(EwArgs a) {
     }
     store4(M + (size_t)r * n, c, n, vec, mm[u]);
     racc = wave_sum(racc);
-    if (lane == 0) d.rowpart[(size_t)t.tj * m + r] = racc;
+    if (lane == 0) gptr(d.rowpart)[(size_t)t.tj * m + r] = racc;
   }
 #pragma unroll
   for (int e = 0; e < 4; ++e) colsh[w][lane * 4 + e] = cacc[e];
@@ -107,7 +108,7 @@ __global__ __launch_bounds__(EW_THREADS) void momentum_rowcol_kernel(EwArgs a) {
     float s = 0.f;
 #pragma unroll
     for (int k = 0; k < NW; ++k) s += colsh[k][cc];
-    d.colpart[(size_t)t.ti * n + col] = s;
+    gptr(d.colpart)[(size_t)t.ti * n + col] = s;
   }
 }
 
@@ -159,16 +160,16 @@ __global__ __launch_bounds__(K2W_THREADS) void scale_convert_wide_kernel(EwArgs 
 #pragma unroll
     for (int e = 0; e < 4; ++e) mm[u][e] = gg[u][e] = 0.f;
     if (rw + u < m) {
-      load4(d.M + (size_t)(rw + u) * n, c, n, vec, mm[u]);
-      if (MALTER) load4(a.ptrs[t.mat].G + (size_t)(rw + u) * n, c, n, vec, gg[u]);
+      load4(gptr(d.M) + (size_t)(rw + u) * n, c, n, vec, mm[u]);
+      if (MALTER) load4(gptr(a.ptrs[t.mat].G) + (size_t)(rw + u) * n, c, n, vec, gg[u]);
     }
   }
-  load4(d.Rv, c, n, true, rv);
+  load4(gptr(d.Rv), c, n, true, rv);
   float s2 = 0.f, q2 = 0.f;
 #pragma unroll
   for (int u = 0; u < RPW; ++u) {
     const int r = rw + u;
-    const float li = r < m ? d.Lv[r] : 0.f;
+    const float li = r < m ? gptr(d.Lv)[r] : 0.f;
     float x[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -181,7 +182,7 @@ __global__ __launch_bounds__(K2W_THREADS) void scale_convert_wide_kernel(EwArgs 
     }
     // X0 is consumed by the next kernel from L2/HBM; streaming store.
     const ew_u32x2 pk = {pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3])};
-    __builtin_nontemporal_store(pk, reinterpret_cast<ew_u32x2*>(d.X[0] + (size_t)r * d.np + c));
+    __builtin_nontemporal_store(pk, reinterpret_cast<MALT_GLOBAL ew_u32x2*>(gptr(d.X[0]) + (size_t)r * d.np + c));
   }
   s2 = wave_sum(s2);
   if (MALTER) q2 = wave_sum(q2);
@@ -197,8 +198,8 @@ __global__ __launch_bounds__(K2W_THREADS) void scale_convert_wide_kernel(EwArgs 
       so += red[0][k];
       sq += red[1][k];
     }
-    d.k2part[2 * (size_t)t.idx + 0] = so;
-    d.k2part[2 * (size_t)t.idx + 1] = sq;
+    gptr(d.k2part)[2 * (size_t)t.idx + 0] = so;
+    gptr(d.k2part)[2 * (size_t)t.idx + 1] = sq;
   }
 }
 
@@ -223,10 +224,10 @@ __global__ __launch_bounds__(K2T_THREADS) void scale_convert_tall_kernel(EwArgs 
   const MatDesc& d = a.desc[t.mat];
   const int m = d.m, n = d.n;
   const bool vec = a.ptrs[t.mat].vec != 0;
-  bf16_t* __restrict__ X0 = d.X[0];
+  MALT_GLOBAL bf16_t* __restrict__ X0 = gptr(d.X[0]);
   const int ldx = d.np;                  // canonical row pitch
-  const float* __restrict__ M = d.M;
-  const float* __restrict__ G = a.ptrs[t.mat].G;
+  const MALT_GLOBAL float* __restrict__ M = gptr(d.M);
+  const MALT_GLOBAL float* __restrict__ G = gptr(a.ptrs[t.mat].G);
   const int r0 = t.ti * K2_T, cb = t.tj * K2_T;   // band columns cb .. cb + TG*K2_T
   const int cc = (threadIdx.x & 15) * 4;          // 4 columns of each tile
   const int rq = threadIdx.x >> 4;                // rows rq + RQ p, p < P
@@ -235,7 +236,7 @@ __global__ __launch_bounds__(K2T_THREADS) void scale_convert_tall_kernel(EwArgs 
 #pragma unroll
   for (int p = 0; p < P; ++p) {
     const int r = r0 + p * RQ + rq;
-    Li[p] = r < m ? d.Lv[r] : 0.f;
+    Li[p] = r < m ? gptr(d.Lv)[r] : 0.f;
   }
   float Rv[TG][4];
 #pragma unroll
@@ -243,7 +244,7 @@ __global__ __launch_bounds__(K2T_THREADS) void scale_convert_tall_kernel(EwArgs 
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int c = cb + j * K2_T + cc + e;
-      Rv[j][e] = c < n ? d.Rv[c] : 0.f;
+      Rv[j][e] = c < n ? gptr(d.Rv)[c] : 0.f;
     }
   float mm[TG][P][4], gg[TG][P][4];
 #pragma unroll
@@ -291,7 +292,7 @@ __global__ __launch_bounds__(K2T_THREADS) void scale_convert_tall_kernel(EwArgs 
   const int seg = (threadIdx.x % SEGS) * SEG;
 #pragma unroll
   for (int j = 0; j < TG; ++j) {
-    ew_u32x4* dst = reinterpret_cast<ew_u32x4*>(X0 + (size_t)(cb + j * K2_T + ct) * ldx + r0 + seg);
+    MALT_GLOBAL ew_u32x4* dst = reinterpret_cast<MALT_GLOBAL ew_u32x4*>(X0 + (size_t)(cb + j * K2_T + ct) * ldx + r0 + seg);
 #pragma unroll
     for (int h = 0; h < SEG / 8; ++h) {
       uint32_t wv[4];
@@ -323,8 +324,8 @@ __global__ __launch_bounds__(K2T_THREADS) void scale_convert_tall_kernel(EwArgs 
       so += red[2 * j][k];
       sq += red[2 * j + 1][k];
     }
-    d.k2part[2 * (size_t)(t.idx + j) + 0] = so;
-    d.k2part[2 * (size_t)(t.idx + j) + 1] = sq;
+    gptr(d.k2part)[2 * (size_t)(t.idx + j) + 0] = so;
+    gptr(d.k2part)[2 * (size_t)(t.idx + j) + 1] = sq;
   }
 }
 
@@ -401,17 +402,17 @@ __global__ __launch_bounds__(EW_THREADS) void backmap_write_kernel(EwArgs a) {
   const bool vec = a.ptrs[t.mat].vec != 0;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int r0 = t.ti * EW_TR, c0 = t.tj * EW_TC, c = c0 + lane * 4;
-  const bf16_t* __restrict__ O = d.X[a.o_parity];
+  const MALT_GLOBAL bf16_t* __restrict__ O = gptr(d.X[a.o_parity]);
   const int ldo = d.np;
-  float* __restrict__ W = a.ptrs[t.mat].W;
-  const float coef = (float)d.scal[SC_COEF];
+  MALT_GLOBAL float* __restrict__ W = gptr(a.ptrs[t.mat].W);
+  const float coef = (float)gptr(d.scal)[SC_COEF];
   const float decay = a.decay;
   if (d.tall) {
     // Canonical rows c0 .. c0+255 (W columns), columns r0 .. r0+31 (W rows):
     // four threads per canonical row, 16 bytes each (inside the padded buffer).
     const int cr = threadIdx.x >> 2, q = threadIdx.x & 3;
     const ew_u32x4 v =
-        __builtin_nontemporal_load(reinterpret_cast<const ew_u32x4*>(O + (size_t)(c0 + cr) * ldo + r0 + q * 8));
+        __builtin_nontemporal_load(reinterpret_cast<const MALT_GLOBAL ew_u32x4*>(O + (size_t)(c0 + cr) * ldo + r0 + q * 8));
     const uint32_t vw[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
@@ -421,7 +422,7 @@ __global__ __launch_bounds__(EW_THREADS) void backmap_write_kernel(EwArgs a) {
     __syncthreads();
   }
   float Rv[4];
-  load4(d.Rv, c, n, true, Rv);
+  load4(gptr(d.Rv), c, n, true, Rv);
   const int rw = r0 + w * RPW;   // this wave's first row
   float wv[RPW][4];
   uint2 pk[RPW];
@@ -430,7 +431,7 @@ __global__ __launch_bounds__(EW_THREADS) void backmap_write_kernel(EwArgs a) {
     if (rw + u < m) {
       load4(W + (size_t)(rw + u) * n, c, n, vec, wv[u]);
       if (!d.tall) {
-        const ew_u32x2 q = __builtin_nontemporal_load(reinterpret_cast<const ew_u32x2*>(O + (size_t)(rw + u) * ldo + c));
+        const ew_u32x2 q = __builtin_nontemporal_load(reinterpret_cast<const MALT_GLOBAL ew_u32x2*>(O + (size_t)(rw + u) * ldo + c));
         pk[u] = make_uint2(q.x, q.y);
       }
     }
@@ -439,7 +440,7 @@ __global__ __launch_bounds__(EW_THREADS) void backmap_write_kernel(EwArgs a) {
   for (int u = 0; u < RPW; ++u) {
     const int r = rw + u;
     if (r >= m) break;   // uniform over the wave
-    const float cl = coef * d.Lv[r];
+    const float cl = coef * gptr(d.Lv)[r];
     float o[4];
     if (!d.tall) {
       o[0] = bf2f((bf16_t)(pk[u].x & 0xffffu));

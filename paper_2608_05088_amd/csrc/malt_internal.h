@@ -43,6 +43,16 @@ constexpr int SM_CH_U = 256;
 
 typedef uint16_t bf16_t;   // bf16 storage
 
+// Device pointers read from the descriptor tables are generic (flat) to the
+// compiler, and flat memory instructions count against lgkmcnt as well as
+// vmcnt: every later wait for an LDS read, a scalar load or a cross-lane
+// shuffle would then also wait for them. Accesses through gptr() are global.
+#define MALT_GLOBAL __attribute__((address_space(1)))
+template <class T>
+__device__ __forceinline__ MALT_GLOBAL T* gptr(T* p) {
+  return (MALT_GLOBAL T*)p;
+}
+
 typedef float malt_f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 malt_bf16x2 __attribute__((ext_vector_type(2)));
 

@@ -441,8 +441,8 @@ void ns_gemm_sym_kernel(NsArgs args) {
       const char* src = lds + row * ST_PITCH_T + ch * 16;
       const uint2 lo = *reinterpret_cast<const uint2*>(src);
       const uint2 hi = *reinterpret_cast<const uint2*>(src + 8);
-      *reinterpret_cast<uint4*>(out + (size_t)(col0 + row) * ldo + off + row0 + ch * 8) =
-          make_uint4(lo.x, lo.y, hi.x, hi.y);
+      const u32x4 v = {lo.x, lo.y, hi.x, hi.y};
+      *reinterpret_cast<MALT_GLOBAL u32x4*>(gptr(out) + (size_t)(col0 + row) * ldo + off + row0 + ch * 8) = v;
     }
     if (!mirror) return;
     __syncthreads();
@@ -473,8 +473,8 @@ void ns_gemm_sym_kernel(NsArgs args) {
 #pragma unroll 4
     for (int c = tid; c < CHUNKS; c += NT) {
       const int row = c >> 5, ch = c & 31;
-      *reinterpret_cast<uint4*>(out + (size_t)(row0 + row) * ldo + off + col0 + ch * 8) =
-          *reinterpret_cast<const uint4*>(lds + row * ST_PITCH_R + ch * 16);
+      *reinterpret_cast<MALT_GLOBAL u32x4*>(gptr(out) + (size_t)(row0 + row) * ldo + off + col0 + ch * 8) =
+          *reinterpret_cast<const u32x4*>(lds + row * ST_PITCH_R + ch * 16);
     }
   };
   emit(0);

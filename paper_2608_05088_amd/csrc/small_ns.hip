@@ -33,10 +33,10 @@ static_assert(SM_CH_G % SM_SUB == 0 && SM_SUB % 8 == 0, "Gram chunk layout");
 // rows 0..SM_M-1, from the momentum (first iteration) or the fp32 iterate.
 __device__ __forceinline__ float sm_x(const MatDesc& d, bool first, const float* Xs, int i, int c, float sig) {
   if (i >= d.mc || c >= d.nc) return 0.f;
-  if (!first) return Xs[(size_t)i * d.np + c];
+  if (!first) return gptr(Xs)[(size_t)i * d.np + c];
   // canonical (i, c) is W(i, c) for wide and W(c, i) for tall matrices
-  if (!d.tall) return sig * d.Lv[i] * d.M[(size_t)i * d.n + c] * d.Rv[c];
-  return sig * d.Lv[c] * d.M[(size_t)c * d.n + i] * d.Rv[i];
+  if (!d.tall) return sig * gptr(d.Lv)[i] * gptr(d.M)[(size_t)i * d.n + c] * gptr(d.Rv)[c];
+  return sig * gptr(d.Lv)[c] * gptr(d.M)[(size_t)c * d.n + i] * gptr(d.Rv)[i];
 }
 
 __global__ __launch_bounds__(NTHREADS) void sm_gram_kernel(NsArgs args) {
@@ -106,7 +106,7 @@ __global__ __launch_bounds__(NTHREADS) void sm_update_kernel(NsArgs args) {
   __shared__ float B[SM_M][SM_M];
   __shared__ float red[2][NTHREADS / 64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (int q = tid; q < SM_M * SM_M; q += NTHREADS) B[q / SM_M][q % SM_M] = d.Bs[q];
+  for (int q = tid; q < SM_M * SM_M; q += NTHREADS) B[q / SM_M][q % SM_M] = gptr(d.Bs)[q];
   const bool first = args.first != 0;
   const float sig = first ? (float)d.scal[SC_SIGMA] : 1.f;
   const int c = t.ti * SM_CH_U + tid;      // canonical column (< np)
@@ -124,7 +124,7 @@ __global__ __launch_bounds__(NTHREADS) void sm_update_kernel(NsArgs args) {
   }
   const int mc = d.mc;
   if (!args.last) {
-    float* Xn = d.Xs[args.src ^ 1];
+    MALT_GLOBAL float* Xn = gptr(d.Xs[args.src ^ 1]);
 #pragma unroll
     for (int i = 0; i < SM_M; ++i)
       if (i < mc) Xn[(size_t)i * d.np + c] = y[i];
@@ -133,9 +133,9 @@ __global__ __launch_bounds__(NTHREADS) void sm_update_kernel(NsArgs args) {
   // Last iteration: O in bf16 where the back-map reads it, and the norms of
   // the rounded values (canonical row i carries the row factor of W for wide
   // and the column factor for tall matrices).
-  bf16_t* O = d.X[args.src ^ 1];
-  const float* const Lm = d.tall ? d.Rv : d.Lv;
-  const float* const Ln = d.tall ? d.Lv : d.Rv;
+  MALT_GLOBAL bf16_t* O = gptr(d.X[args.src ^ 1]);
+  const MALT_GLOBAL float* const Lm = gptr(d.tall ? d.Rv : d.Lv);
+  const MALT_GLOBAL float* const Ln = gptr(d.tall ? d.Lv : d.Rv);
   const float ln = c < d.nc ? Ln[c] : 0.f;
   float o2 = 0.f, d2 = 0.f;
 #pragma unroll
@@ -168,8 +168,8 @@ __global__ __launch_bounds__(NTHREADS) void sm_update_kernel(NsArgs args) {
       so += red[0][w];
       sd += red[1][w];
     }
-    d.gpart[2 * (size_t)t.idx + 0] = so;
-    d.gpart[2 * (size_t)t.idx + 1] = sd;
+    gptr(d.gpart)[2 * (size_t)t.idx + 0] = so;
+    gptr(d.gpart)[2 * (size_t)t.idx + 1] = sd;
   }
 }
 
