@@ -115,7 +115,9 @@ malt_status_t malt_state_size(const malt_shape_t* shapes, int32_t n, malt_varian
  * from_existing = 1: adopt the state already in `state_mem` (resume from a
  *   checkpoint) and set t = `step` (the number of steps already taken).
  * Uploads descriptor tables into the workspace on `stream` and synchronises
- * that stream before returning.  On success *out owns a new plan. */
+ * that stream before returning.  The device that owns the buffers and the
+ * stream must be current (it also receives the kernels' LDS limit).  On
+ * success *out owns a new plan. */
 malt_status_t malt_init_state(malt_plan_t** out, const malt_shape_t* shapes, int32_t n,
                               malt_variant_t variant, void* state_mem, void* workspace_mem,
                               int32_t from_existing, int64_t step, void* stream);

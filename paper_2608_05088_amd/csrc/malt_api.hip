@@ -474,6 +474,11 @@ malt_status_t malt_init_state(malt_plan_t** out, const malt_shape_t* shapes, int
     delete p;
     return fail(MALT_ERR_ALIAS, "state and workspace buffers overlap");
   }
+  // Device work starts here, after every argument check.
+  {
+    const hipError_t e = ns_gemm_setup();
+    if (e != hipSuccess) { delete p; return hip_fail(e, "setting the Newton-Schulz kernels' LDS limit"); }
+  }
   p->variant = variant;
   p->n = n;
   p->shapes.assign(shapes, shapes + n);

@@ -726,16 +726,20 @@ void ns_update_kernel(NsArgs args) {
   }
 }
 
+// Both kernels use more dynamic LDS than the default limit; the attribute is
+// set for the current device (plan set-up calls this with the plan's device
+// current, so every device a plan runs on has it).
+hipError_t ns_gemm_setup() {
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&ns_gemm_sym_kernel),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
+  if (e == hipSuccess)
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&ns_update_kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
+  return e;
+}
+
 hipError_t launch_ns_gemm(const NsArgs& a, hipStream_t s) {
   if (a.ntiles == 0) return hipSuccess;
-  static bool attr_set = false;
-  if (!attr_set) {
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&ns_gemm_sym_kernel),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
-    (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&ns_update_kernel),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
-    attr_set = true;
-  }
   if (a.phase == PH_UPDATE)
     hipLaunchKernelGGL(ns_update_kernel, dim3(a.ntiles), dim3(NT), LDS_BYTES, s, a);
   else

@@ -180,10 +180,11 @@ class Plan:
         self.workspace = torch.empty(wb, dtype=torch.uint8, device=self.device)
         self._c_shapes = _shapes(self.shapes)
         handle = c_void_p()
-        _check(lib().malt_init_state(ctypes.byref(handle), self._c_shapes, len(self.shapes),
-                                     VARIANTS[variant], c_void_p(self.state.data_ptr()),
-                                     c_void_p(self.workspace.data_ptr()), int(from_existing),
-                                     int(step), c_void_p(_stream_handle(stream))))
+        with torch.cuda.device(self.device):   # the plan's device is current during set-up
+            _check(lib().malt_init_state(ctypes.byref(handle), self._c_shapes, len(self.shapes),
+                                         VARIANTS[variant], c_void_p(self.state.data_ptr()),
+                                         c_void_p(self.workspace.data_ptr()), int(from_existing),
+                                         int(step), c_void_p(_stream_handle(stream))))
         self._h = handle
 
     # -- stepping ----------------------------------------------------------------
