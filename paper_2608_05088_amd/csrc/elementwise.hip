@@ -116,24 +116,31 @@ __global__ __launch_bounds__(EW_THREADS) void momentum_rowcol_kernel(EwArgs a) {
 // Row / column EMAs and the diagonal preconditioners.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(NTHREADS) void precond_finalize_kernel(EwArgs a) {
+  // Tile (mat, 0 = rows | 1 = columns, chunk): FIN_W rows or columns, each
+  // summed by FIN_SPLIT threads (every FIN_SPLIT-th partial, in order), the
+  // thread sums combined in a fixed order.
+  constexpr int SPLIT = NTHREADS / FIN_W;
+  static_assert(SPLIT == 4, "pairwise combine of four sums");
+  __shared__ double part[SPLIT][FIN_W];
   const Tile t = a.tiles[blockIdx.x];
   const MatDesc& d = a.desc[t.mat];
-  const int i = t.tj * NTHREADS + threadIdx.x;
-  if (t.ti == 0) {
-    if (i >= d.m) return;
-    double s = 0.0;
-    for (int c = 0; c < d.k1_ct; ++c) s += (double)d.rowpart[(size_t)c * d.m + i];
-    const double lv = a.mu2 * (double)d.l[i] + (1.0 - a.mu2) * s;
-    d.l[i] = (float)lv;
-    d.Lv[i] = a.identity ? 1.f : (float)pow(lv + a.eps, -0.125);
-  } else {
-    if (i >= d.n) return;
-    double s = 0.0;
-    for (int c = 0; c < d.k1_rt; ++c) s += (double)d.colpart[(size_t)c * d.n + i];
-    const double rv = a.mu2 * (double)d.r[i] + (1.0 - a.mu2) * s;
-    d.r[i] = (float)rv;
-    d.Rv[i] = a.identity ? 1.f : (float)pow(rv + a.eps, -0.125);
-  }
+  const bool rows = t.ti == 0;
+  const int len = rows ? d.m : d.n, nparts = rows ? d.k1_ct : d.k1_rt;
+  const MALT_GLOBAL float* const src = gptr(rows ? d.rowpart : d.colpart);
+  const int g = threadIdx.x / FIN_W, j = threadIdx.x % FIN_W;
+  const int i = t.tj * FIN_W + j;
+  double s = 0.0;
+  if (i < len)
+    for (int c = g; c < nparts; c += SPLIT) s += (double)src[(size_t)c * len + i];
+  part[g][j] = s;
+  __syncthreads();
+  if (g != 0 || i >= len) return;
+  const double sum = (part[0][j] + part[1][j]) + (part[2][j] + part[3][j]);
+  float* const ema = rows ? d.l : d.r;
+  float* const inv = rows ? d.Lv : d.Rv;
+  const double v = a.mu2 * (double)gptr(ema)[i] + (1.0 - a.mu2) * sum;
+  gptr(ema)[i] = (float)v;
+  gptr(inv)[i] = a.identity ? 1.f : (float)pow(v + a.eps, -0.125);
 }
 
 // ---------------------------------------------------------------------------

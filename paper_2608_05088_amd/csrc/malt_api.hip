@@ -187,8 +187,8 @@ void build_tiles(const Layout& L, std::vector<Tile>& ew, std::vector<Tile>& fin,
     const MatPlan& q = L.mats[i];
     for (int32_t ti = 0; ti < q.k1_rt; ++ti)
       for (int32_t tj = 0; tj < q.k1_ct; ++tj) ew.push_back({i, ti, tj, 0});
-    for (int32_t c = 0; c < cdiv(q.m, NTHREADS); ++c) fin.push_back({i, 0, c, 0});
-    for (int32_t c = 0; c < cdiv(q.n, NTHREADS); ++c) fin.push_back({i, 1, c, 0});
+    for (int32_t c = 0; c < cdiv(q.m, FIN_W); ++c) fin.push_back({i, 0, c, 0});
+    for (int32_t c = 0; c < cdiv(q.n, FIN_W); ++c) fin.push_back({i, 1, c, 0});
     if (q.small) {
       for (int32_t c = 0; c < q.sm_gchunks; ++c) smg.push_back({i, c, 0, 0});
       smp.push_back({i, 0, 0, 0});
@@ -249,7 +249,7 @@ Layout make_layout(const malt_shape_t* shapes, int32_t n, malt_variant_t variant
     p.upd_tiles = p.small ? p.np / SM_CH_U : T * (p.np / NS_TILE);
     p.ns_flops_sym_per_iter = 3.0 * double(p.mc) * p.mc * p.nc + double(p.mc) * p.mc * p.mc;
     L.n_ew += p.k1_rt * p.k1_ct;
-    L.n_fin += cdiv(p.m, NTHREADS) + cdiv(p.n, NTHREADS);
+    L.n_fin += cdiv(p.m, FIN_W) + cdiv(p.n, FIN_W);
     L.n_k2 += p.k2_tiles;
     if (!p.tall) L.n_k2w += p.k2_tiles;
     if (p.small) {

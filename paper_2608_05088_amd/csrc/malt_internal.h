@@ -34,6 +34,8 @@ constexpr int NS_BK = 64;
 constexpr int NS_SPLIT_MAX = 128;
 // Threads of every workgroup.
 constexpr int NTHREADS = 256;
+// Preconditioner finalise: rows or columns per workgroup (4 threads each).
+constexpr int FIN_W = 64;
 // Matrices whose short side is at most this run Newton-Schulz in fp32 (X, A
 // and B' kept in fp32): Gram partials over SM_CH_G columns per workgroup,
 // updates over SM_CH_U columns (one per thread).
