@@ -181,8 +181,8 @@ def cpu_baseline(w, layers: int):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (the step shards by whole matrices; see the design notes); "
-              f"--gpus {args.gpus} is not supported", file=sys.stderr)
+        print(f"bench.py measures one GPU only: across GPUs the step would shard by whole matrices, which "
+              f"libmalt does not implement; --gpus {args.gpus} is not supported", file=sys.stderr)
         sys.exit(2)
     import torch
 
