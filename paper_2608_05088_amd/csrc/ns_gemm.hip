@@ -290,8 +290,15 @@ void ns_gemm_sym_kernel(NsArgs args) {
   // the row panel only and reads both operands from it.
   const bool diag = t.ti == t.tj;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wr = wave / (NW / 2), wc = wave % (NW / 2);
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // Sub-tile of each wave. On a diagonal tile only the 32 x 32 blocks on or
+  // above the block diagonal are computed (the others are their mirrors). The
+  // two waves that share a SIMD (waves w and w + 4) then take sub-tiles with
+  // 8 + 0, 8 + 0, 7 + 3 and 3 + 7 such blocks, instead of the 3 + 0, 7 + 0,
+  // 8 + 3 and 8 + 7 of the plain order, so every matrix core gets a share.
+  static_assert(NW != 8 || (TM == 128 && TN == 64), "diagonal sub-tile pairing assumes a 2 x 4 wave grid");
+  const int role = (NW == 8 && diag) ? ((0x76540132u >> (4 * wave)) & 0xF) : wave;
+  const int wr = role / (NW / 2), wc = role % (NW / 2);
 
   // Direct-load sources: instruction g < LOADS_PER_OPER covers rows of the
   // tile-row panel, the rest rows of the tile-column panel (both of P); byte
@@ -330,37 +337,46 @@ void ns_gemm_sym_kernel(NsArgs args) {
   // With 8 waves, g = wave + 8q < LOADS_PER_OPER exactly for q < LOADS / 2:
   // the first half of a wave's loads are row-panel loads.
   static_assert(LOADS_PER_OPER == (LOADS / 2) * NW, "row-panel loads are the first half");
-  pipeline(
-      K / BK, diag ? LOADS / 2 : LOADS, lds,
-      [&](int kt, int i) {   // diagonal tiles issue the row-panel loads q < LOADS / 2 only
-        dma16(rsP, voff[i], (uint32_t)(kt * BK * 2), lds_u32(lds + (kt % STAGES) * STAGE_BYTES + dst_off[i]));
-      },
-      [&](int buf, const char* st, int h) {
+  // Diagonal and off-diagonal tiles run separate copies of the main loop, so
+  // the block test exists only on diagonal tiles.
+  auto main_loop = [&](auto diag_tag) {
+    constexpr bool DIAG = decltype(diag_tag)::value;
+    pipeline(
+        K / BK, DIAG ? LOADS / 2 : LOADS, lds,
+        [&](int kt, int i) {   // diagonal tiles issue the row-panel loads q < LOADS / 2 only
+          dma16(rsP, voff[i], (uint32_t)(kt * BK * 2), lds_u32(lds + (kt % STAGES) * STAGE_BYTES + dst_off[i]));
+        },
+        [&](int buf, const char* st, int h) {
 #pragma unroll
-        for (int i = 0; i < I; ++i) fa[buf][i] = *reinterpret_cast<const bf16x8*>(st + offa[i][h]);
+          for (int i = 0; i < I; ++i) fa[buf][i] = *reinterpret_cast<const bf16x8*>(st + offa[i][h]);
 #pragma unroll
-        for (int j = 0; j < J; ++j) fb[buf][j] = *reinterpret_cast<const bf16x8*>(st + offb[j][h]);
-      },
-      [&](int buf, auto&& after) {
+          for (int j = 0; j < J; ++j) fb[buf][j] = *reinterpret_cast<const bf16x8*>(st + offb[j][h]);
+        },
+        [&](int buf, auto&& after) {
 #pragma unroll
-        for (int i = 0; i < I; ++i)
+          for (int i = 0; i < I; ++i)
 #pragma unroll
-          for (int j = 0; j < J; ++j) {
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[buf][i], fb[buf][j], acc[i][j], 0, 0, 0);
-            after(i * J + j);
-          }
-      });
+            for (int j = 0; j < J; ++j) {
+              // Diagonal tiles skip the blocks below the block diagonal.
+              if (!DIAG || (wr * TM) / 32 + i <= (wc * TN) / 32 + j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[buf][i], fb[buf][j], acc[i][j], 0, 0, 0);
+              after(i * J + j);
+            }
+        });
+  };
+  if (diag) main_loop(std::true_type{});
+  else main_loop(std::false_type{});
 
   // ---------------------------------------------------------------- epilogue
   // acc[i][j][4g + e] = C(r, c): tile row r = wr*TM + i*32 + 8g + 4*(lane >> 5)
   // + e, tile column c = wc*TN + j*32 + (lane & 31), so each lane holds four
   // consecutive rows of one column.  The final bf16 values are formed in
   // registers; the tile then leaves through LDS twice in whole rows: first
-  // transposed (the mirror tile C^T, or the tile itself on the diagonal),
-  // then, for off-diagonal tiles, as is after a 4 x 4 transpose inside each
-  // lane quad.
+  // transposed (the mirror tile C^T), then as is after a 4 x 4 transpose
+  // inside each lane quad. A diagonal tile is its own mirror and leaves once:
+  // its staged copy takes the computed blocks transposed and the blocks above
+  // the block diagonal as is, so it is symmetric by construction.
   const bool poly = phase == PH_POLY;
-  const bool mirror = t.ti != t.tj;
   const float sc = sig * sig;
   // Split B': the low part bf16(v - hi) goes mp columns to the right.
   const int lo_off = (poly && split) ? mp : 0;
@@ -420,21 +436,51 @@ void ns_gemm_sym_kernel(NsArgs args) {
         }
   }
 
+  // Row-wise copy of accumulator group (i, j, g): a 4 x 4 transpose of
+  // 16-bit values inside each lane quad, after which lane p of the quad holds
+  // row p of the quad's four rows, its four columns.
+  const int p = lane & 3;
+  auto quad_rows = [&](int i, int j, int g) {
+    const uint32_t A0 = hv[i][j][g].x, B0 = hv[i][j][g].y;   // rows (0,1), (2,3) of column p
+    const uint32_t A1 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)A0, 0xB1, 0xF, 0xF, true);   // lane p ^ 1
+    const uint32_t B1 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)B0, 0xB1, 0xF, 0xF, true);
+    // Even lanes: row 0 (A) / row 2 (B) at columns p, p+1; odd lanes:
+    // row 1 / row 3 at columns p-1, p.
+    const uint32_t nA = (p & 1) ? ((A1 >> 16) | (A0 & 0xffff0000u)) : ((A0 & 0xffffu) | (A1 << 16));
+    const uint32_t nB = (p & 1) ? ((B1 >> 16) | (B0 & 0xffff0000u)) : ((B0 & 0xffffu) | (B1 << 16));
+    const uint32_t S = (p < 2) ? nB : nA;
+    const uint32_t S2 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)S, 0x4E, 0xF, 0xF, true);   // lane p ^ 2
+    return (p < 2) ? make_uint2(nA, S2) : make_uint2(S2, nB);
+  };
   // Writes one set of values (hi, or the split low part at column offset
   // off): the transposed staging first, then the row-wise one.
   auto emit = [&](int off) {
     constexpr int CHUNKS = NS_TILE * NS_TILE * 2 / 16;
     __syncthreads();   // LDS free (A's tile read, or the previous copy-out done)
+    // Transposed staging: staged row x is tile column x. A diagonal tile
+    // stages only its computed blocks this way (block row <= block column) and
+    // stages the blocks above the block diagonal also as is, at the places of
+    // their skipped mirrors: the staged tile is then the whole symmetric tile.
 #pragma unroll
     for (int i = 0; i < I; ++i)
 #pragma unroll
-      for (int j = 0; j < J; ++j)
+      for (int j = 0; j < J; ++j) {
+        const int br = (wr * TM) / 32 + i, bc = (wc * TN) / 32 + j;   // wave-uniform block coordinates
+        if (!diag || br <= bc)
 #pragma unroll
-        for (int g = 0; g < 4; ++g)
-          *reinterpret_cast<uint2*>(lds + (cl0 + j * 32) * ST_PITCH_T + (rl0 + i * 32 + 8 * g) * 2) = hv[i][j][g];
+          for (int g = 0; g < 4; ++g)
+            *reinterpret_cast<uint2*>(lds + (cl0 + j * 32) * ST_PITCH_T + (rl0 + i * 32 + 8 * g) * 2) = hv[i][j][g];
+        if (diag && br < bc)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const int rr = rl0 + i * 32 + 8 * g + p;
+            const int cc = wc * TN + j * 32 + ((lane & 31) & ~3);
+            *reinterpret_cast<uint2*>(lds + rr * ST_PITCH_T + cc * 2) = quad_rows(i, j, g);
+          }
+      }
     __syncthreads();
-    // Staged row x is tile column x: it goes to row col0 + x (the mirror
-    // tile; on the diagonal, col0 = row0 and it is the tile itself).
+    // Staged row x goes to row col0 + x (the mirror tile; on a diagonal tile,
+    // the tile itself).
 #pragma unroll 4
     for (int c = tid; c < CHUNKS; c += NT) {
       const int row = c >> 5, ch = c & 31;
@@ -444,30 +490,17 @@ void ns_gemm_sym_kernel(NsArgs args) {
       const u32x4 v = {lo.x, lo.y, hi.x, hi.y};
       *reinterpret_cast<MALT_GLOBAL u32x4*>(gptr(out) + (size_t)(col0 + row) * ldo + off + row0 + ch * 8) = v;
     }
-    if (!mirror) return;
+    if (diag) return;
     __syncthreads();
-    // 4 x 4 transpose of 16-bit values inside each lane quad: lane p of the
-    // quad ends with row p of the quad's four rows, its four columns.
-    const int p = lane & 3;
 #pragma unroll
     for (int i = 0; i < I; ++i)
 #pragma unroll
       for (int j = 0; j < J; ++j)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const uint32_t A0 = hv[i][j][g].x, B0 = hv[i][j][g].y;   // rows (0,1), (2,3) of column p
-          const uint32_t A1 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)A0, 0xB1, 0xF, 0xF, true);   // lane p ^ 1
-          const uint32_t B1 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)B0, 0xB1, 0xF, 0xF, true);
-          // Even lanes: row 0 (A) / row 2 (B) at columns p, p+1; odd lanes:
-          // row 1 / row 3 at columns p-1, p.
-          const uint32_t nA = (p & 1) ? ((A1 >> 16) | (A0 & 0xffff0000u)) : ((A0 & 0xffffu) | (A1 << 16));
-          const uint32_t nB = (p & 1) ? ((B1 >> 16) | (B0 & 0xffff0000u)) : ((B0 & 0xffffu) | (B1 << 16));
-          const uint32_t S = (p < 2) ? nB : nA;
-          const uint32_t S2 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)S, 0x4E, 0xF, 0xF, true);   // lane p ^ 2
-          const uint2 rowv = (p < 2) ? make_uint2(nA, S2) : make_uint2(S2, nB);
           const int rr = rl0 + i * 32 + 8 * g + p;
           const int cc = wc * TN + j * 32 + ((lane & 31) & ~3);
-          *reinterpret_cast<uint2*>(lds + rr * ST_PITCH_R + cc * 2) = rowv;
+          *reinterpret_cast<uint2*>(lds + rr * ST_PITCH_R + cc * 2) = quad_rows(i, j, g);
         }
     __syncthreads();
 #pragma unroll 4
