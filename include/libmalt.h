@@ -148,11 +148,17 @@ malt_status_t malt_state_layout(const malt_plan_t* plan, int32_t i, malt_state_l
  *  X0:      bf16 L M R before normalisation, same layout; valid only after a
  *           step with ns_steps == 1 (later iterations reuse the buffer);
  *  scalars: float64 [s=||Mt||_F, sigma=1/(s+ns_eps), nu_t, alpha_t, ||O||^2,
- *           ||D||^2, graft=||O||/(||D||+eps), coef=lr*alpha*graft]. */
+ *           ||D||^2, graft=||O||/(||D||+eps), coef=lr*alpha*graft];
+ *  A, B:    bf16 last Newton-Schulz iteration's A = X X^T and B' = a I + b A
+ *           + c A A (symmetric, m' x m' padded to AB_pitch = a multiple of 256
+ *           rows and columns); B holds [B'_hi | B'_lo] with row pitch
+ *           2 AB_pitch when B_split = 1. Unused (0) for matrices with a short
+ *           side of at most 32, whose Newton-Schulz runs in fp32. */
 typedef struct {
   int64_t Lv, Rv, O, X0, scalars;
   int64_t O_pitch;
   int64_t O_transposed;
+  int64_t A, B, AB_pitch, B_split;
 } malt_debug_layout_t;
 malt_status_t malt_debug_layout(const malt_plan_t* plan, int32_t i, malt_debug_layout_t* out);
 

@@ -709,6 +709,10 @@ malt_status_t malt_debug_layout(const malt_plan_t* p, int32_t i, malt_debug_layo
   out->O_pitch = q.np;
   out->O_transposed = q.tall ? 1 : 0;
   out->scalars = int64_t(q.ws_scal);
+  out->A = q.small ? 0 : int64_t(q.ws_A);
+  out->B = q.small ? 0 : int64_t(q.ws_B);
+  out->AB_pitch = q.small ? 0 : q.mp;
+  out->B_split = q.split ? 1 : 0;
   return MALT_OK;
 }
 

@@ -52,7 +52,8 @@ class malt_state_layout_t(ctypes.Structure):
 
 class malt_debug_layout_t(ctypes.Structure):
     _fields_ = [("Lv", c_int64), ("Rv", c_int64), ("O", c_int64), ("X0", c_int64),
-                ("scalars", c_int64), ("O_pitch", c_int64), ("O_transposed", c_int64)]
+                ("scalars", c_int64), ("O_pitch", c_int64), ("O_transposed", c_int64),
+                ("A", c_int64), ("B", c_int64), ("AB_pitch", c_int64), ("B_split", c_int64)]
 
 
 class malt_profile_t(ctypes.Structure):
@@ -256,10 +257,19 @@ class Plan:
             return canon.t() if L.O_transposed else canon
 
         sc = w[L.scalars: L.scalars + 8 * 16].view(torch.float64)
-        return {"Lv": w[L.Lv: L.Lv + 4 * m].view(torch.float32),
-                "Rv": w[L.Rv: L.Rv + 4 * n].view(torch.float32),
-                "O": bf16(L.O), "X0": bf16(L.X0),
-                "scalars": {k: sc[j] for j, k in enumerate(SCALAR_NAMES)}}
+        views = {"Lv": w[L.Lv: L.Lv + 4 * m].view(torch.float32),
+                 "Rv": w[L.Rv: L.Rv + 4 * n].view(torch.float32),
+                 "O": bf16(L.O), "X0": bf16(L.X0),
+                 "scalars": {k: sc[j] for j, k in enumerate(SCALAR_NAMES)}}
+        if L.AB_pitch:   # bf16 Newton-Schulz path: the last iteration's A and B' (padded)
+            p = L.AB_pitch
+            views["A"] = w[L.A: L.A + 2 * p * p].view(torch.bfloat16).view(p, p)
+            bw = 2 * p if L.B_split else p
+            b = w[L.B: L.B + 2 * p * bw].view(torch.bfloat16).view(p, bw)
+            views["B"] = b[:, :p]
+            if L.B_split:
+                views["B_lo"] = b[:, p:]
+        return views
 
     # -- profiling ---------------------------------------------------------------
     def profile_enable(self, enable: bool = True) -> None:

@@ -218,6 +218,36 @@ def test_scale_convert_is_bitexact_rne(variant):
         assert np.array_equal(got, _bf16_rne(x)), f"matrix {i}: bf16 conversion differs from RNE"
 
 
+@pytest.mark.parametrize("variant", ["malt", "malter"])
+def test_gram_and_polynomial_outputs_are_exactly_symmetric(variant):
+    # A = X X^T and B' = a I + b A + c A A are symmetric. Diagonal tiles compute
+    # only their blocks on and above the block diagonal and stage the rest as
+    # the mirror, so both buffers must equal their transposes bitwise
+    # (padding included). Shapes: 3 x 3 tiles (diagonal and off-diagonal), a
+    # tall matrix, a 1280-square matrix and a split one (m' <= 128: B' as
+    # [hi | lo]).
+    import torch
+    shapes = [(700, 1500), (1500, 300), (1280, 1280), (64, 5000)]
+    say(f"[parity] A and B' exactly symmetric {variant} {shapes}")
+    W0 = [wl.weight(95, i, s) for i, s in enumerate(shapes)]
+    G = [wl.grad(95, 1, i, s, "row_loguniform") for i, s in enumerate(shapes)]
+    plan = lm.Plan(shapes, variant)
+    Wd, Gd = to_dev(W0), to_dev(G)
+    plan.step(Wd, Gd, lm.make_hparams(lr=1e-2))
+    torch.cuda.synchronize()
+    for i, (m, n) in enumerate(shapes):
+        dv = plan.debug_views(i)
+        for key in ("A", "B", "B_lo"):
+            if key not in dv:
+                continue
+            x = dv[key].contiguous().view(torch.int16)
+            assert torch.equal(x, x.t().contiguous()), f"matrix {i} ({m}x{n}): {key} is not exactly symmetric"
+        mc = min(m, n)
+        a = dv["A"][:mc, :mc].float()
+        assert float(a.abs().max().item()) > 0.0 and bool(torch.isfinite(a).all().item())
+        assert float(dv["A"][mc:, :].abs().max().item() if dv["A"].shape[0] > mc else 0.0) == 0.0
+
+
 # Four shape kinds (a split contraction with K = 2 m', unsplit K = 768, a tall
 # matrix, a wide split one) repeated: 496 update tiles, more than one per
 # compute unit, of different K and pitch in one grouped launch.
