@@ -174,3 +174,36 @@ def test_non_finite_gradient_stays_in_its_matrix():
     for k in (0, 1, 3):
         assert np.array_equal(outs[0][k], outs[1][k])
     assert not np.all(np.isfinite(outs[1][2]))
+
+
+def test_concurrent_plans_on_two_streams_match_a_single_plan():
+    # Plans share no device state: two plans stepping at the same time on two
+    # streams (default priority) give bitwise the results of one plan alone.
+    import torch
+    shapes = [(700, 1500), (1500, 300), (64, 5000), (20, 3000)]
+    say(f"[runtime] two plans on two streams {shapes}")
+    W0 = [wl.weight(94, i, s) for i, s in enumerate(shapes)]
+    grads = [[wl.grad(94, t, i, s, "row_loguniform") for i, s in enumerate(shapes)] for t in (1, 2, 3)]
+    hp = lm.make_hparams(lr=3e-3)
+
+    ref = lm.Plan(shapes, "malter")
+    Wr = to_dev(W0)
+    for g in grads:
+        ref.step(Wr, to_dev(g), hp)
+    torch.cuda.synchronize()
+
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    plans = [lm.Plan(shapes, "malter", stream=st) for st in streams]
+    Ws = [to_dev(W0), to_dev(W0)]
+    Gs = [[to_dev(g) for g in grads], [to_dev(g) for g in grads]]
+    torch.cuda.synchronize()
+    for t in range(len(grads)):
+        for k in range(2):
+            with torch.cuda.stream(streams[k]):
+                plans[k].step(Ws[k], Gs[k][t], hp, stream=streams[k])
+    torch.cuda.synchronize()
+    for k in range(2):
+        for i in range(len(shapes)):
+            assert torch.equal(Ws[k][i], Wr[i]), f"plan {k}, matrix {i} differs from the single-plan run"
+    for pl in plans + [ref]:
+        pl.close()
