@@ -66,11 +66,14 @@ constexpr int LOADS = 2 * OPER_BYTES / 1024 / NW;    // 1 KB direct loads per wa
 // of one column, 8 bytes into one staged row) uses rows padded by 8 bytes, so
 // the 32 staged rows of one write land in distinct banks; a tile written
 // row-wise (each lane: four consecutive columns) uses rows padded by 64 bytes.
-// The update keeps its per-tile norm partials past the staged tile.
+// The update instead stages each wave's sub-tile (128 rows of 64 bf16 when
+// NW = 8) in a region of its own, rows padded by 8 bytes, and keeps its
+// per-tile norm partials past the NW regions.
 constexpr int ST_PITCH_T = NS_TILE * 2 + 8;
 constexpr int ST_PITCH_R = NS_TILE * 2 + 64;
-constexpr int UPD_PITCH = ST_PITCH_T;
-constexpr int UPD_RED = NS_TILE * UPD_PITCH;
+constexpr int UPD_PITCH = NS_TILE / (NW / 2) * 2 + 8;
+constexpr int UPD_WAVE = NS_TILE / 2 * UPD_PITCH;
+constexpr int UPD_RED = NW * UPD_WAVE;
 constexpr int UPD_EPI_BYTES = UPD_RED + 2 * NW * 4;
 constexpr int SYM_EPI_BYTES = NS_TILE * ST_PITCH_R;
 constexpr int EPI_BYTES = UPD_EPI_BYTES > SYM_EPI_BYTES ? UPD_EPI_BYTES : SYM_EPI_BYTES;
@@ -651,11 +654,14 @@ void ns_update_kernel(NsArgs args) {
   // ---------------------------------------------------------------- epilogue
   // acc[a][b][4g + e] = C(m, n + e), m = row0 + wr*TM + b*32 + (lane & 31),
   // n = col0 + wc*TN + a*32 + 8g + 4*(lane >> 5): four consecutive bf16 per
-  // lane.  They go to an LDS copy of the tile first; the tile then leaves in
-  // whole 512-byte rows (16 bytes per lane), not as 16-byte pieces of 32 rows.
+  // lane.  Each wave copies its own TM x TN sub-tile to a private LDS region
+  // and writes it out in whole 128-byte row pieces, not as 16-byte pieces of
+  // 32 rows.  A wave reads back only what it staged, so no barrier separates
+  // the two and each wave leaves the epilogue at its own pace.
   const int ml0 = wr * TM + (lane & 31);          // tile-local row of b = 0
   const int nl0 = wc * TN + 4 * (lane >> 5);      // tile-local column of a = g = 0
-  char* const sto = lds;
+  const int sr0 = lane & 31, sc0 = 4 * (lane >> 5);   // the same within the sub-tile
+  char* const sto = lds + wave * UPD_WAVE;
   __syncthreads();   // every wave is done reading the operand ring
   float o2 = 0.f, d2 = 0.f;
   if (!args.last) {
@@ -668,7 +674,7 @@ void ns_update_kernel(NsArgs args) {
           uint2 pk;
           pk.x = pack_bf16x2(sc * acc[a][b][4 * g + 0], sc * acc[a][b][4 * g + 1]);
           pk.y = pack_bf16x2(sc * acc[a][b][4 * g + 2], sc * acc[a][b][4 * g + 3]);
-          *reinterpret_cast<uint2*>(sto + (ml0 + b * 32) * UPD_PITCH + (nl0 + a * 32 + 8 * g) * 2) = pk;
+          *reinterpret_cast<uint2*>(sto + (sr0 + b * 32) * UPD_PITCH + (sc0 + a * 32 + 8 * g) * 2) = pk;
         }
   } else {
     // Last iteration: also the per-tile sums of O^2 and (L O R)^2, from the
@@ -703,7 +709,7 @@ void ns_update_kernel(NsArgs args) {
           uint2 pk;
           pk.x = pack_bf16x2(sc * acc[a][b][4 * g + 0], sc * acc[a][b][4 * g + 1]);
           pk.y = pack_bf16x2(sc * acc[a][b][4 * g + 2], sc * acc[a][b][4 * g + 3]);
-          *reinterpret_cast<uint2*>(sto + (ml0 + b * 32) * UPD_PITCH + nl * 2) = pk;
+          *reinterpret_cast<uint2*>(sto + (sr0 + b * 32) * UPD_PITCH + (sc0 + a * 32 + 8 * g) * 2) = pk;
           const float ov[4] = {bf16_lo(pk.x), bf16_hi(pk.x), bf16_lo(pk.y), bf16_hi(pk.y)};
           float rowo = 0.f, rowd = 0.f;
 #pragma unroll
@@ -721,24 +727,25 @@ void ns_update_kernel(NsArgs args) {
       }
     }
   }
-  __syncthreads();
-  // Copy-out: 256 rows x 32 chunks of 16 bytes; a wave writes two whole rows
-  // per store.  Each chunk is read as two 8-byte halves (rows are 8-byte
-  // aligned in the padded copy).
-  constexpr int CHUNKS = NS_TILE * NS_TILE * 2 / 16;
-#pragma unroll 4
-  for (int c = tid; c < CHUNKS; c += NT) {
-    const int row = c >> 5, ch = c & 31;
-    const char* src = sto + row * UPD_PITCH + ch * 16;
+  // Copy-out: TM rows x TN/8 chunks of 16 bytes; one store covers 512 / TN
+  // rows.  Each chunk is read as two 8-byte halves (rows are 8-byte aligned
+  // in the padded copy).  Streaming store: the next kernel reads X' from
+  // another XCD's L2 anyway, and the operand panels keep this one.
+  constexpr int SCH = TN * 2 / 16;   // chunks per staged row
+  static_assert(TM * SCH % 64 == 0, "whole stores per wave");
+#pragma unroll
+  for (int it = 0; it < TM * SCH / 64; ++it) {
+    const int q = lane + 64 * it;
+    const int r = q / SCH, ch = q % SCH;
+    const char* src = sto + r * UPD_PITCH + ch * 16;
     const uint2 lo = *reinterpret_cast<const uint2*>(src);
     const uint2 hi = *reinterpret_cast<const uint2*>(src + 8);
-    // Streaming store: the next kernel reads X' from another XCD's L2 anyway,
-    // and the operand panels keep this one.
     const u32x4 v = {lo.x, lo.y, hi.x, hi.y};
-    __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(Xn + (size_t)(row0 + row) * np + col0 + ch * 8));
+    __builtin_nontemporal_store(
+        v, reinterpret_cast<MALT_GLOBAL u32x4*>(gptr(Xn) + (size_t)(row0 + wr * TM + r) * np + col0 + wc * TN + ch * 8));
   }
   if (!args.last) return;
-  // Deterministic per-tile sums for the graft norms (LDS past the staged tile).
+  // Deterministic per-tile sums for the graft norms (LDS past the staged sub-tiles).
   float* red = reinterpret_cast<float*>(lds + UPD_RED);
   o2 = wsum(o2);
   d2 = wsum(d2);
