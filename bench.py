@@ -68,7 +68,8 @@ def recorded_traffic(workload: str):
 
 def small_case_latency(lm, wl, dev, reps: int = 50):
     """Latency of one step on the single 256 x 512 matrix workload (MALT),
-    which is bound by launch latency, not by bandwidth or matrix-core rate:
+    which is bound by kernel latency (one or two workgroups per launch), not by
+    bandwidth or matrix-core rate:
     median over `reps` individually timed steps."""
     import statistics
 
