@@ -74,11 +74,19 @@ constexpr int ST_PITCH_R = NS_TILE * 2 + 64;
 constexpr int UPD_PITCH = NS_TILE / (NW / 2) * 2 + 8;
 constexpr int UPD_WAVE = NS_TILE / 2 * UPD_PITCH;
 constexpr int UPD_RED = NW * UPD_WAVE;
+// Off-diagonal Gram/polynomial tiles also go through per-wave regions: the
+// sub-tile transposed (TN rows of TM bf16, padded by 8 bytes), then as is (TM
+// rows of TN bf16, unpadded, halves swapped on alternate row pairs).
+constexpr int SYM_PITCH_T = NS_TILE / 2 * 2 + 8;
+constexpr int SYM_WAVE = (NS_TILE / (NW / 2)) * SYM_PITCH_T > (NS_TILE / 2) * (NS_TILE / (NW / 2)) * 2
+                             ? (NS_TILE / (NW / 2)) * SYM_PITCH_T
+                             : (NS_TILE / 2) * (NS_TILE / (NW / 2)) * 2;
 constexpr int UPD_EPI_BYTES = UPD_RED + 2 * NW * 4;
 constexpr int SYM_EPI_BYTES = NS_TILE * ST_PITCH_R;
 constexpr int EPI_BYTES = UPD_EPI_BYTES > SYM_EPI_BYTES ? UPD_EPI_BYTES : SYM_EPI_BYTES;
 constexpr int LDS_BYTES = RING_BYTES > EPI_BYTES ? RING_BYTES : EPI_BYTES;
 static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
+static_assert(NW * SYM_WAVE <= LDS_BYTES && UPD_RED + 2 * NW * 4 <= LDS_BYTES, "per-wave epilogue regions");
 static_assert(H % 2 == 0, "sub-steps per stage must be even");
 static_assert(LOADS * NW * 1024 == 2 * OPER_BYTES, "loads must split evenly over the waves");
 
@@ -460,6 +468,63 @@ void ns_gemm_sym_kernel(NsArgs args) {
   auto emit = [&](int off) {
     constexpr int CHUNKS = NS_TILE * NS_TILE * 2 / 16;
     __syncthreads();   // LDS free (A's tile read, or the previous copy-out done)
+    if constexpr (TM == 128 && TN == 64) {   // the layout below assumes 128 x 64 wave blocks
+      if (!diag) {
+        // Off-diagonal tile: each wave moves its own TM x TN block through a
+        // private LDS region, first transposed (to the mirror tile), then as
+        // is.  A wave reads back only what it wrote and LDS operations of one
+        // wave stay in order, so no barrier separates the phases.  Outputs are
+        // written with streaming stores, as in the update: the next phase
+        // reads them from other XCDs.
+        char* const wreg = lds + wave * SYM_WAVE;
+#pragma unroll
+        for (int i = 0; i < I; ++i)
+#pragma unroll
+          for (int j = 0; j < J; ++j)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+              *reinterpret_cast<uint2*>(wreg + ((lane & 31) + j * 32) * SYM_PITCH_T +
+                                        (4 * (lane >> 5) + i * 32 + 8 * g) * 2) = hv[i][j][g];
+        // Mirror: staged row x (of TM bf16) goes to row col0 + wc*TN + x.
+        constexpr int TCH = TM * 2 / 16;
+#pragma unroll
+        for (int it = 0; it < TN * TCH / 64; ++it) {
+          const int q = lane + 64 * it;
+          const int r = q / TCH, ch = q % TCH;
+          const char* src = wreg + r * SYM_PITCH_T + ch * 16;
+          const uint2 lo = *reinterpret_cast<const uint2*>(src);
+          const uint2 hi = *reinterpret_cast<const uint2*>(src + 8);
+          const u32x4 v = {lo.x, lo.y, hi.x, hi.y};
+          __builtin_nontemporal_store(v, reinterpret_cast<MALT_GLOBAL u32x4*>(
+                                             gptr(out) + (size_t)(col0 + wc * TN + r) * ldo + off + row0 + wr * TM + ch * 8));
+        }
+        // As is: 128-byte rows; rows 2 and 3 (mod 4) hold their two 64-byte
+        // halves swapped, so the four rows of one quad write land in four
+        // distinct 16-bank groups.
+#pragma unroll
+        for (int i = 0; i < I; ++i)
+#pragma unroll
+          for (int j = 0; j < J; ++j)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+              const int r = 4 * (lane >> 5) + i * 32 + 8 * g + p;
+              const int hf = j ^ ((r >> 1) & 1);
+              *reinterpret_cast<uint2*>(wreg + r * (TN * 2) + hf * 64 + (((lane & 31) >> 2) << 3)) =
+                  quad_rows(i, j, g);
+            }
+        constexpr int DCH = TN * 2 / 16;
+#pragma unroll
+        for (int it = 0; it < TM * DCH / 64; ++it) {
+          const int q = lane + 64 * it;
+          const int r = q / DCH, ch = q % DCH;
+          const int hf = (ch >> 2) ^ ((r >> 1) & 1);
+          const u32x4 v = *reinterpret_cast<const u32x4*>(wreg + r * (TN * 2) + hf * 64 + (ch & 3) * 16);
+          __builtin_nontemporal_store(v, reinterpret_cast<MALT_GLOBAL u32x4*>(
+                                             gptr(out) + (size_t)(row0 + wr * TM + r) * ldo + off + col0 + wc * TN + ch * 8));
+        }
+        return;
+      }
+    }
     // Transposed staging: staged row x is tile column x. A diagonal tile
     // stages only its computed blocks this way (block row <= block column) and
     // stages the blocks above the block diagonal also as is, at the places of
@@ -491,7 +556,8 @@ void ns_gemm_sym_kernel(NsArgs args) {
       const uint2 lo = *reinterpret_cast<const uint2*>(src);
       const uint2 hi = *reinterpret_cast<const uint2*>(src + 8);
       const u32x4 v = {lo.x, lo.y, hi.x, hi.y};
-      *reinterpret_cast<MALT_GLOBAL u32x4*>(gptr(out) + (size_t)(col0 + row) * ldo + off + row0 + ch * 8) = v;
+      __builtin_nontemporal_store(
+          v, reinterpret_cast<MALT_GLOBAL u32x4*>(gptr(out) + (size_t)(col0 + row) * ldo + off + row0 + ch * 8));
     }
     if (diag) return;
     __syncthreads();
@@ -509,8 +575,9 @@ void ns_gemm_sym_kernel(NsArgs args) {
 #pragma unroll 4
     for (int c = tid; c < CHUNKS; c += NT) {
       const int row = c >> 5, ch = c & 31;
-      *reinterpret_cast<MALT_GLOBAL u32x4*>(gptr(out) + (size_t)(row0 + row) * ldo + off + col0 + ch * 8) =
-          *reinterpret_cast<const u32x4*>(lds + row * ST_PITCH_R + ch * 16);
+      __builtin_nontemporal_store(*reinterpret_cast<const u32x4*>(lds + row * ST_PITCH_R + ch * 16),
+                                  reinterpret_cast<MALT_GLOBAL u32x4*>(gptr(out) + (size_t)(row0 + row) * ldo + off +
+                                                                       col0 + ch * 8));
     }
   };
   emit(0);
