@@ -262,6 +262,16 @@ __device__ __forceinline__ void pipeline(const int KT, const int nl, char* lds, 
           }
         }
       });
+      // Alternate the sub-step's MFMAs with the fragment reads for the next
+      // one, so each read's latency is covered by this wave's own MFMAs (left
+      // to itself the scheduler puts the reads after the last MFMA and the
+      // next sub-step then waits for them).
+#pragma unroll
+      for (int j = 0; j < NMMA; ++j) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
   constexpr int LEAD = SPREAD ? STAGES - 1 : STAGES;
