@@ -196,7 +196,7 @@ constexpr int NMMA = (TM / 32) * (TN / 32);   // MFMAs per wave per sub-step
 constexpr bool SPREAD = MALT_NS_SPREAD != 0;
 static_assert(!SPREAD || STAGES >= 3, "spread loads need two stages of lead");
 
-template <class Issue, class Read, class Mma>
+template <int RPM, class Issue, class Read, class Mma>
 __device__ __forceinline__ void pipeline(const int KT, const int nl, char* lds, Issue&& issue, Read&& read,
                                          Mma&& mma) {
   constexpr int PRE = SPREAD ? STAGES - 1 : STAGES;   // stages loaded before the loop
@@ -262,14 +262,14 @@ __device__ __forceinline__ void pipeline(const int KT, const int nl, char* lds, 
           }
         }
       });
-      // Alternate the sub-step's MFMAs with the fragment reads for the next
-      // one, so each read's latency is covered by this wave's own MFMAs (left
-      // to itself the scheduler puts the reads after the last MFMA and the
-      // next sub-step then waits for them).
+      // Interleave the sub-step's MFMAs with the fragment reads for the next
+      // one, RPM reads after each MFMA, so each read's latency is covered by
+      // this wave's own MFMAs (left to itself the scheduler puts the reads
+      // after the last MFMA and the next sub-step then waits for them).
 #pragma unroll
       for (int j = 0; j < NMMA; ++j) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, RPM, 0);   // RPM LDS reads
       }
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -362,7 +362,7 @@ void ns_gemm_sym_kernel(NsArgs args) {
   // the block test exists only on diagonal tiles.
   auto main_loop = [&](auto diag_tag) {
     constexpr bool DIAG = decltype(diag_tag)::value;
-    pipeline(
+    pipeline<1>(
         K / BK, DIAG ? LOADS / 2 : LOADS, lds,
         [&](int kt, int i) {   // diagonal tiles issue the row-panel loads q < LOADS / 2 only
           dma16(rsP, voff[i], (uint32_t)(kt * BK * 2), lds_u32(lds + (kt % STAGES) * STAGE_BYTES + dst_off[i]));
@@ -697,7 +697,7 @@ void ns_update_kernel(NsArgs args) {
       for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.f;
   bf16x8 fx[2][NA], fb[2][NB];
 
-  pipeline(
+  pipeline<2>(
       K / BK, LOADS, lds,
       [&](int kt, int q) {   // q < LOADS / 2: B' rows, else X k-rows
         const int k0 = kt * BK;
