@@ -26,7 +26,8 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 matrix-core peak
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ns_update_gpt2_large_traffic.md")
-NS_SOURCE = os.path.join(ROOT, "paper_2608_05088_amd", "csrc", "ns_gemm.hip")
+# The update kernel is built from ns_gemm.hip with the stage geometry ns_update.hip sets.
+NS_SOURCES = [os.path.join(ROOT, "paper_2608_05088_amd", "csrc", f) for f in ("ns_gemm.hip", "ns_update.hip")]
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
 METRIC = "MALT step latency (ms) per GPT-2 param set; NS MFMA % bf16 peak; HBM GB/s"
 
@@ -60,7 +61,7 @@ def recorded_traffic(workload: str):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             fields[k.strip().lstrip("- ").strip("`")] = v.strip().strip("`")
-    sha = hashlib.sha256(open(NS_SOURCE, "rb").read()).hexdigest()
+    sha = hashlib.sha256(b"".join(open(f, "rb").read() for f in NS_SOURCES)).hexdigest()
     if fields.get("source_sha256") != sha or "traffic_bytes_per_launch" not in fields:
         return None
     return float(fields["traffic_bytes_per_launch"])

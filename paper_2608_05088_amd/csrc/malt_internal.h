@@ -171,6 +171,8 @@ hipError_t launch_graft_scalars(const EwArgs& a, int32_t nmat, hipStream_t s);
 hipError_t launch_backmap_write(const EwArgs& a, hipStream_t s);
 hipError_t ns_gemm_setup();   // once per plan, on the plan's device
 hipError_t launch_ns_gemm(const NsArgs& a, hipStream_t s);
+hipError_t ns_update_setup();   // the update kernel (ns_update.hip), called by ns_gemm_setup
+hipError_t launch_ns_update(const NsArgs& a, hipStream_t s);
 hipError_t launch_small_ns(const NsArgs& a, hipStream_t s);
 
 // XCDs of the chip; workgroups are dispatched to them round-robin.

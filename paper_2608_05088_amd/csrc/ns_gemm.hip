@@ -280,6 +280,7 @@ __device__ __forceinline__ void pipeline(const int KT, const int nl, char* lds, 
   for (; kt < KT; ++kt) body(kt, std::false_type{});
 }
 
+#ifndef MALT_NS_UPDATE_TU
 // ===========================================================================
 // Gram and polynomial phases: C = P Q^T, symmetric output, upper tiles.
 // ===========================================================================
@@ -605,6 +606,7 @@ void ns_gemm_sym_kernel(NsArgs args) {
   }
 }
 
+#else
 // ===========================================================================
 // Update phase: X' = s B' X  (NN), computed as C^T = X^T B'^T blocks.
 // ===========================================================================
@@ -843,25 +845,35 @@ void ns_update_kernel(NsArgs args) {
   }
 }
 
-// Both kernels use more dynamic LDS than the default limit; the attribute is
-// set for the current device (plan set-up calls this with the plan's device
-// current, so every device a plan runs on has it).
+#endif
+
+// Each kernel uses more dynamic LDS than the default limit; the attribute is
+// set for the current device (plan set-up calls ns_gemm_setup with the plan's
+// device current, so every device a plan runs on has it).
+#ifdef MALT_NS_UPDATE_TU
+hipError_t ns_update_setup() {
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(&ns_update_kernel),
+                             hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
+}
+
+hipError_t launch_ns_update(const NsArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(ns_update_kernel, dim3(a.ntiles), dim3(NT), LDS_BYTES, s, a);
+  return hipGetLastError();
+}
+#else
 hipError_t ns_gemm_setup() {
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&ns_gemm_sym_kernel),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
-  if (e == hipSuccess)
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&ns_update_kernel),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
+  if (e == hipSuccess) e = ns_update_setup();
   return e;
 }
 
 hipError_t launch_ns_gemm(const NsArgs& a, hipStream_t s) {
   if (a.ntiles == 0) return hipSuccess;
-  if (a.phase == PH_UPDATE)
-    hipLaunchKernelGGL(ns_update_kernel, dim3(a.ntiles), dim3(NT), LDS_BYTES, s, a);
-  else
-    hipLaunchKernelGGL(ns_gemm_sym_kernel, dim3(a.ntiles), dim3(NT), LDS_BYTES, s, a);
+  if (a.phase == PH_UPDATE) return launch_ns_update(a, s);
+  hipLaunchKernelGGL(ns_gemm_sym_kernel, dim3(a.ntiles), dim3(NT), LDS_BYTES, s, a);
   return hipGetLastError();
 }
+#endif
 
 }  // namespace malt
