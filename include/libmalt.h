@@ -32,7 +32,7 @@
  *    rounded up to multiples of 256.  Device pointers must be 4-byte aligned; rows whose
  *    start is 16-byte aligned with cols % 4 == 0 take a vectorised path.
  *  - All device memory is owned by the caller.  The library never allocates
- *    device memory (it allocates a little pinned host memory at init).
+ *    device or pinned host memory.
  *  - `stream` is a hipStream_t (NULL = the legacy default stream).  Steps are
  *    enqueued asynchronously; argument errors are detected on the host before
  *    anything is enqueued and leave the state untouched.
@@ -87,8 +87,11 @@ typedef struct {
   int32_t precond_identity;    /* 1: L = R = I (the step is then Muon's, Sec. 3.1) */
 } malt_hparams_t;
 
-/* Paper defaults: lr 1.3e-3, mu1 0.95, mu2 0.99, eps 1e-8, weight_decay 0,
- * ns_steps 5, (ns_a, ns_b, ns_c) = (3.4445, -4.7750, 2.0315), ns_eps 1e-7. */
+/* Defaults: lr 1.3e-3, mu1 0.95, mu2 0.99, eps 1e-8 (the paper's
+ * hyper-parameter table), weight_decay 0 (a reading: the table lists 0.1 but
+ * Algorithms 1 and 2 have no decay term; 0 reproduces them exactly),
+ * ns_steps 5, (ns_a, ns_b, ns_c) = (3.4445, -4.7750, 2.0315), ns_eps 1e-7
+ * (Muon's published Newton-Schulz settings; the paper gives none). */
 void malt_hparams_default(malt_hparams_t* hp);
 
 /* Opaque host-side plan: shapes, shape groups, device descriptor tables and
@@ -127,7 +130,11 @@ malt_status_t malt_init_state(malt_plan_t** out, const malt_shape_t* shapes, int
  * grads[i]:  device float32 rows x cols, read only.
  * shapes/n must equal the init shapes (else MALT_ERR_STATE_MISMATCH).
  * Increments t on success; bias corrections use the new t.  Returns after
- * enqueueing: the caller synchronises `stream` before reading results. */
+ * enqueueing, without waiting on the host for anything: the caller
+ * synchronises `stream` before reading results.  When a param or grad pointer
+ * differs from the previous step's, the plan's device pointer table is first
+ * rewritten by small kernels on `stream` (the pointers travel as kernel
+ * arguments). */
 malt_status_t malt_step(malt_plan_t* plan, float* const* params, const float* const* grads,
                         const malt_shape_t* shapes, int32_t n, const malt_hparams_t* hp,
                         void* stream);
@@ -182,7 +189,7 @@ typedef struct {
 malt_status_t malt_profile_enable(malt_plan_t* plan, int32_t enable);
 malt_status_t malt_profile_read(malt_plan_t* plan, malt_profile_t* out, int32_t reset);
 
-/* Release the plan (host memory and events only). */
+/* Release the plan (host memory and profiling events only). */
 void malt_destroy_state(malt_plan_t* plan);
 
 const char* malt_status_string(malt_status_t status);

@@ -475,6 +475,48 @@ __global__ __launch_bounds__(EW_THREADS) void backmap_write_kernel(EwArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Plan plumbing: the pointer table of a step, and zeroing of device buffers
+// (a kernel rather than a memset node, so either can sit in a captured graph).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(PTR_CHUNK) void ptr_upload_kernel(PtrUploadArgs a) {
+  const int i = threadIdx.x;
+  if (i < a.count) {
+    // Field by field: PtrPair is 24 bytes, written as three 8-byte words.
+    const uint64_t* src = reinterpret_cast<const uint64_t*>(&a.p[i]);
+    MALT_GLOBAL uint64_t* dst = reinterpret_cast<MALT_GLOBAL uint64_t*>(gptr(a.dst + i));
+    static_assert(sizeof(PtrPair) == 24, "pointer table entry layout");
+    dst[0] = src[0];
+    dst[1] = src[1];
+    dst[2] = src[2];
+  }
+}
+
+__global__ __launch_bounds__(NTHREADS) void zero_fill_kernel(ew_u32x4* dst, size_t n16, uint8_t* tail, int ntail) {
+  const ew_u32x4 z = {0u, 0u, 0u, 0u};
+  for (size_t i = (size_t)blockIdx.x * NTHREADS + threadIdx.x; i < n16; i += (size_t)gridDim.x * NTHREADS)
+    gptr(dst)[i] = z;
+  if (blockIdx.x == 0 && (int)threadIdx.x < ntail) gptr(tail)[threadIdx.x] = 0;
+}
+
+hipError_t launch_ptr_upload(const PtrUploadArgs& a, hipStream_t s) {
+  if (a.count <= 0 || a.count > PTR_CHUNK) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(ptr_upload_kernel, dim3(1), dim3(PTR_CHUNK), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_fill(void* dst, size_t bytes, hipStream_t s) {
+  if (bytes == 0) return hipSuccess;
+  if (reinterpret_cast<uintptr_t>(dst) % 16 != 0) return hipErrorInvalidValue;
+  const size_t n16 = bytes / 16;
+  const int ntail = int(bytes % 16);
+  const size_t want = (n16 + NTHREADS - 1) / NTHREADS;
+  const unsigned grid = unsigned(want < 4096 ? (want > 0 ? want : 1) : 4096);
+  hipLaunchKernelGGL(zero_fill_kernel, dim3(grid), dim3(NTHREADS), 0, s, reinterpret_cast<ew_u32x4*>(dst), n16,
+                     static_cast<uint8_t*>(dst) + n16 * 16, ntail);
+  return hipGetLastError();
+}
+
 hipError_t launch_momentum_rowcol(const EwArgs& a, hipStream_t s) {
   if (a.ntiles == 0) return hipSuccess;
   hipLaunchKernelGGL(momentum_rowcol_kernel, dim3(a.ntiles), dim3(EW_THREADS), 0, s, a);

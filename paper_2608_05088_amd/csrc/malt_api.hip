@@ -321,12 +321,9 @@ struct malt_plan {
   char* state = nullptr;
   char* ws = nullptr;
   int64_t t = 0;
-  // pointer table staging
-  PtrPair* h_ptrs = nullptr;          // pinned
+  // pointer table last written to the workspace (compared on every step)
   std::vector<PtrPair> cur_ptrs;
   bool ptrs_valid = false;
-  hipEvent_t ptr_ev = nullptr;
-  bool ptr_ev_recorded = false;
   // profiling
   bool prof = false;
   struct EvSet { std::vector<hipEvent_t> ev; std::vector<int> phase; };
@@ -418,6 +415,71 @@ void fill_desc(const malt_plan* p, std::vector<MatDesc>& D) {
   }
 }
 
+malt_status_t check_init_args(const malt_shape_t* shapes, int32_t n, malt_variant_t variant, void* state_mem,
+                              int32_t from_existing, int64_t step) {
+  if (variant != MALT_VARIANT_MALT && variant != MALT_VARIANT_MALTER)
+    return fail(MALT_ERR_INVALID_ARG, "unknown variant %d", int(variant));
+  malt_status_t st = check_shapes(shapes, n);
+  if (st != MALT_OK) return st;
+  if (!state_mem) return fail(MALT_ERR_INVALID_ARG, "state pointer is NULL");
+  if (reinterpret_cast<uintptr_t>(state_mem) % 16 != 0)
+    return fail(MALT_ERR_ALIGNMENT, "state_mem must be 16-byte aligned");
+  if (from_existing != 0 && from_existing != 1) return fail(MALT_ERR_INVALID_ARG, "from_existing must be 0 or 1");
+  if (from_existing && step < 0) return fail(MALT_ERR_INVALID_ARG, "step must be >= 0");
+  return MALT_OK;
+}
+
+// Lays the plan over state_mem and ws (p->L already set): uploads the
+// descriptor table and work lists, zeroes the workspace (and the state unless
+// resuming), and synchronises the stream.  Allocates no device or pinned host
+// memory.
+malt_status_t init_plan(malt_plan* p, const malt_shape_t* shapes, int32_t n, malt_variant_t variant,
+                        void* state_mem, char* ws, int32_t from_existing, int64_t step, void* stream) {
+  if (ranges_overlap(reinterpret_cast<uintptr_t>(state_mem), p->L.state_bytes, reinterpret_cast<uintptr_t>(ws),
+                     p->L.ws_bytes))
+    return fail(MALT_ERR_ALIAS, "state and workspace buffers overlap");
+  // Device work starts here, after every argument check.
+  hipError_t e = ns_gemm_setup();
+  if (e != hipSuccess) return hip_fail(e, "setting the Newton-Schulz kernels' LDS limit");
+  p->variant = variant;
+  p->n = n;
+  p->shapes.assign(shapes, shapes + n);
+  p->state = static_cast<char*>(state_mem);
+  p->ws = ws;
+  p->t = from_existing ? step : 0;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  std::vector<MatDesc> D;
+  fill_desc(p, D);
+  std::vector<Tile> ew, fin, k2, sym, upd, smg, smp, smu;
+  build_tiles(p->L, ew, fin, k2, sym, upd, smg, smp, smu);
+  std::vector<Tile> gram, poly, updd;
+  ns_dispatch_lists(p->L, sym, upd, gram, poly, updd);
+
+  // Every table in one host image of the workspace head.
+  const size_t head = p->L.ws_t_smu + sizeof(Tile) * smu.size();
+  std::vector<char> h(head, 0);
+  char* hc = h.data();
+  memcpy(hc + p->L.ws_desc, D.data(), sizeof(MatDesc) * n);
+  memcpy(hc + p->L.ws_t_ew, ew.data(), sizeof(Tile) * ew.size());
+  memcpy(hc + p->L.ws_t_fin, fin.data(), sizeof(Tile) * fin.size());
+  memcpy(hc + p->L.ws_t_k2, k2.data(), sizeof(Tile) * k2.size());
+  memcpy(hc + p->L.ws_t_gram, gram.data(), sizeof(Tile) * gram.size());
+  memcpy(hc + p->L.ws_t_poly, poly.data(), sizeof(Tile) * poly.size());
+  memcpy(hc + p->L.ws_t_upd, updd.data(), sizeof(Tile) * updd.size());
+  memcpy(hc + p->L.ws_t_smg, smg.data(), sizeof(Tile) * smg.size());
+  memcpy(hc + p->L.ws_t_smp, smp.data(), sizeof(Tile) * smp.size());
+  memcpy(hc + p->L.ws_t_smu, smu.data(), sizeof(Tile) * smu.size());
+
+  e = launch_zero_fill(p->ws, p->L.ws_bytes, s);
+  if (e == hipSuccess) e = hipMemcpyAsync(p->ws, hc, head, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess && !from_existing) e = launch_zero_fill(p->state, p->L.state_bytes, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "uploading plan tables");
+  p->cur_ptrs.assign(n, PtrPair{nullptr, nullptr, 0, 0});
+  return MALT_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -455,75 +517,15 @@ malt_status_t malt_init_state(malt_plan_t** out, const malt_shape_t* shapes, int
                               int32_t from_existing, int64_t step, void* stream) {
   if (!out) return fail(MALT_ERR_INVALID_ARG, "out is NULL");
   *out = nullptr;
-  if (variant != MALT_VARIANT_MALT && variant != MALT_VARIANT_MALTER)
-    return fail(MALT_ERR_INVALID_ARG, "unknown variant %d", int(variant));
-  malt_status_t st = check_shapes(shapes, n);
+  malt_status_t st = check_init_args(shapes, n, variant, state_mem, from_existing, step);
   if (st != MALT_OK) return st;
-  if (!state_mem || !workspace_mem) return fail(MALT_ERR_INVALID_ARG, "state or workspace pointer is NULL");
-  if (reinterpret_cast<uintptr_t>(state_mem) % 16 != 0)
-    return fail(MALT_ERR_ALIGNMENT, "state_mem must be 16-byte aligned");
+  if (!workspace_mem) return fail(MALT_ERR_INVALID_ARG, "workspace pointer is NULL");
   if (reinterpret_cast<uintptr_t>(workspace_mem) % 256 != 0)
     return fail(MALT_ERR_ALIGNMENT, "workspace_mem must be 256-byte aligned");
-  if (from_existing != 0 && from_existing != 1) return fail(MALT_ERR_INVALID_ARG, "from_existing must be 0 or 1");
-  if (from_existing && step < 0) return fail(MALT_ERR_INVALID_ARG, "step must be >= 0");
-
   malt_plan* p = new malt_plan();
   p->L = make_layout(shapes, n, variant);
-  if (ranges_overlap(reinterpret_cast<uintptr_t>(state_mem), p->L.state_bytes,
-                     reinterpret_cast<uintptr_t>(workspace_mem), p->L.ws_bytes)) {
-    delete p;
-    return fail(MALT_ERR_ALIAS, "state and workspace buffers overlap");
-  }
-  // Device work starts here, after every argument check.
-  {
-    const hipError_t e = ns_gemm_setup();
-    if (e != hipSuccess) { delete p; return hip_fail(e, "setting the Newton-Schulz kernels' LDS limit"); }
-  }
-  p->variant = variant;
-  p->n = n;
-  p->shapes.assign(shapes, shapes + n);
-  p->state = static_cast<char*>(state_mem);
-  p->ws = static_cast<char*>(workspace_mem);
-  p->t = from_existing ? step : 0;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-
-  std::vector<MatDesc> D;
-  fill_desc(p, D);
-  std::vector<Tile> ew, fin, k2, sym, upd, smg, smp, smu;
-  build_tiles(p->L, ew, fin, k2, sym, upd, smg, smp, smu);
-  std::vector<Tile> gram, poly, updd;
-  ns_dispatch_lists(p->L, sym, upd, gram, poly, updd);
-
-  // Stage every table in one pinned buffer laid out like the workspace head.
-  const size_t head = p->L.ws_t_smu + sizeof(Tile) * smu.size();
-  void* h = nullptr;
-  hipError_t e = hipHostMalloc(&h, head, hipHostMallocDefault);
-  if (e != hipSuccess) { delete p; return hip_fail(e, "hipHostMalloc"); }
-  memset(h, 0, head);
-  char* hc = static_cast<char*>(h);
-  memcpy(hc + p->L.ws_desc, D.data(), sizeof(MatDesc) * n);
-  memcpy(hc + p->L.ws_t_ew, ew.data(), sizeof(Tile) * ew.size());
-  memcpy(hc + p->L.ws_t_fin, fin.data(), sizeof(Tile) * fin.size());
-  memcpy(hc + p->L.ws_t_k2, k2.data(), sizeof(Tile) * k2.size());
-  memcpy(hc + p->L.ws_t_gram, gram.data(), sizeof(Tile) * gram.size());
-  memcpy(hc + p->L.ws_t_poly, poly.data(), sizeof(Tile) * poly.size());
-  memcpy(hc + p->L.ws_t_upd, updd.data(), sizeof(Tile) * updd.size());
-  memcpy(hc + p->L.ws_t_smg, smg.data(), sizeof(Tile) * smg.size());
-  memcpy(hc + p->L.ws_t_smp, smp.data(), sizeof(Tile) * smp.size());
-  memcpy(hc + p->L.ws_t_smu, smu.data(), sizeof(Tile) * smu.size());
-
-  e = hipMemsetAsync(p->ws, 0, p->L.ws_bytes, s);
-  if (e == hipSuccess) e = hipMemcpyAsync(p->ws, hc, head, hipMemcpyHostToDevice, s);
-  if (e == hipSuccess && !from_existing) e = hipMemsetAsync(p->state, 0, p->L.state_bytes, s);
-  if (e == hipSuccess) e = hipStreamSynchronize(s);
-  (void)hipHostFree(h);
-  if (e != hipSuccess) { delete p; return hip_fail(e, "uploading plan tables"); }
-
-  e = hipHostMalloc(reinterpret_cast<void**>(&p->h_ptrs), sizeof(PtrPair) * n, hipHostMallocDefault);
-  if (e != hipSuccess) { delete p; return hip_fail(e, "hipHostMalloc"); }
-  e = hipEventCreateWithFlags(&p->ptr_ev, hipEventDisableTiming);
-  if (e != hipSuccess) { (void)hipHostFree(p->h_ptrs); delete p; return hip_fail(e, "hipEventCreate"); }
-  p->cur_ptrs.assign(n, PtrPair{nullptr, nullptr, 0, 0});
+  st = init_plan(p, shapes, n, variant, state_mem, static_cast<char*>(workspace_mem), from_existing, step, stream);
+  if (st != MALT_OK) { delete p; return st; }
   *out = p;
   return MALT_OK;
 }
@@ -568,25 +570,31 @@ malt_status_t malt_step(malt_plan_t* p, float* const* params, const float* const
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e;
   if (changed) {
-    if (p->ptr_ev_recorded) {
-      e = hipEventSynchronize(p->ptr_ev);   // previous upload has left the staging buffer
-      if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
-    }
+    // The new table travels in the arguments of small copy kernels, which the
+    // runtime captures at enqueue: nothing on the host waits.
+    PtrUploadArgs up;
+    up.count = 0;
+    std::vector<PtrPair> next(n);
     for (int32_t i = 0; i < n; ++i) {
       // The vectorised elementwise path needs 16-byte aligned rows of W, G and M.
       const MatPlan& q = p->L.mats[i];
       const uintptr_t M = reinterpret_cast<uintptr_t>(p->state) + 4 * size_t(q.st_M);
-      p->h_ptrs[i].W = params[i];
-      p->h_ptrs[i].G = grads[i];
-      p->h_ptrs[i].vec = (q.n % 4 == 0) && (reinterpret_cast<uintptr_t>(params[i]) % 16 == 0) &&
-                         (reinterpret_cast<uintptr_t>(grads[i]) % 16 == 0) && (M % 16 == 0);
-      p->h_ptrs[i].pad_ = 0;
-      p->cur_ptrs[i] = p->h_ptrs[i];
+      next[i].W = params[i];
+      next[i].G = grads[i];
+      next[i].vec = (q.n % 4 == 0) && (reinterpret_cast<uintptr_t>(params[i]) % 16 == 0) &&
+                    (reinterpret_cast<uintptr_t>(grads[i]) % 16 == 0) && (M % 16 == 0);
+      next[i].pad_ = 0;
     }
-    e = hipMemcpyAsync(p->ws + p->L.ws_ptrs, p->h_ptrs, sizeof(PtrPair) * n, hipMemcpyHostToDevice, s);
-    if (e == hipSuccess) e = hipEventRecord(p->ptr_ev, s);
+    PtrPair* dst = reinterpret_cast<PtrPair*>(p->ws + p->L.ws_ptrs);
+    e = hipSuccess;
+    for (int32_t i0 = 0; i0 < n && e == hipSuccess; i0 += PTR_CHUNK) {
+      up.dst = dst + i0;
+      up.count = std::min<int32_t>(PTR_CHUNK, n - i0);
+      memcpy(up.p, next.data() + i0, sizeof(PtrPair) * up.count);
+      e = launch_ptr_upload(up, s);
+    }
     if (e != hipSuccess) { p->ptrs_valid = false; return hip_fail(e, "uploading pointer table"); }
-    p->ptr_ev_recorded = true;
+    p->cur_ptrs = next;
     p->ptrs_valid = true;
   }
 
@@ -757,11 +765,6 @@ void malt_destroy_state(malt_plan_t* p) {
   if (!p) return;
   (void)drain_profile(p);
   for (hipEvent_t ev : p->free_events) (void)hipEventDestroy(ev);
-  if (p->ptr_ev) {
-    if (p->ptr_ev_recorded) (void)hipEventSynchronize(p->ptr_ev);
-    (void)hipEventDestroy(p->ptr_ev);
-  }
-  if (p->h_ptrs) (void)hipHostFree(p->h_ptrs);
   delete p;
 }
 

@@ -162,7 +162,19 @@ struct NsArgs {
   float a, b, c;
 };
 
+// Per-step pointer table written by a kernel whose arguments carry the
+// pointers: the runtime copies kernel arguments at enqueue, so a step needs no
+// host staging buffer and never waits for an earlier upload.
+constexpr int PTR_CHUNK = 128;
+struct PtrUploadArgs {
+  PtrPair* dst;
+  int32_t count;       // <= PTR_CHUNK
+  PtrPair p[PTR_CHUNK];
+};
+
 // Launchers (stream-ordered, no synchronisation).
+hipError_t launch_ptr_upload(const PtrUploadArgs& a, hipStream_t s);
+hipError_t launch_zero_fill(void* dst, size_t bytes, hipStream_t s);   // dst 16-byte aligned
 hipError_t launch_momentum_rowcol(const EwArgs& a, hipStream_t s);
 hipError_t launch_precond_finalize(const EwArgs& a, hipStream_t s);
 hipError_t launch_scale_convert(const EwArgs& a, bool tall, hipStream_t s);

@@ -87,6 +87,69 @@ def run_gpu(shapes, variant: str, W0: Sequence[np.ndarray], grads: Sequence[Sequ
     return out
 
 
+def run_sampled_against_oracle(w, steps: int, sample: Sequence[int], hp_kw: dict, label: str,
+                               tol_ns: float = TOL_NS, tol_state: float = TOL_STATE) -> Dict[str, float]:
+    """Step every matrix of workload `w` for `steps` steps in one plan (the
+    benchmark's launch configuration) and compare the sampled matrices with the
+    oracle after every step (the oracle runs in lockstep, so host memory holds
+    one step at a time).  The sampled matrices get the host generator's weights
+    and gradients (the oracle's inputs); the others get device-drawn ones, which
+    cannot affect the sampled matrices: the step is independent per matrix."""
+    import torch
+
+    from paper_2608_05088_amd import workloads as wl
+    dev = torch_dev()
+    shapes = list(w.shapes)
+    sample = list(sample)
+    plan = lm.Plan(shapes, w.variant)
+    hp = lm.make_hparams(**hp_kw)
+    W0h = {i: wl.weight(w.cid, i, shapes[i]) for i in sample}
+    Wd = [torch.from_numpy(W0h[i]).to(dev) if i in W0h else wl.weight_device(w.cid, i, s, dev)
+          for i, s in enumerate(shapes)]
+    Gd = [torch.empty(s, dtype=torch.float32, device=dev) for s in shapes]
+    sub = [shapes[i] for i in sample]
+    ost = oracle_init(sub, w.variant)
+    ohp = OracleHparams(variant=w.variant, **hp_kw)
+    Wo = [W0h[i].astype(np.float64) for i in sample]
+    worst: Dict[str, float] = {}
+    for t in range(1, steps + 1):
+        gh = {}
+        for i, s in enumerate(shapes):
+            if i in W0h:
+                gh[i] = wl.grad(w.cid, t, i, s, w.dist)
+                Gd[i].copy_(torch.from_numpy(gh[i]))
+            else:
+                wl.grad_device(w.cid, t, i, s, w.dist, dev, out=Gd[i])
+        before = [Wd[i].double().cpu().numpy() for i in sample]
+        plan.step(Wd, Gd, hp)
+        torch.cuda.synchronize()
+        st = GpuStep([], [], [], [], [], [], [], [], [], [], [])
+        for k, i in enumerate(sample):
+            M, l, r, nu = plan.state_views(i)
+            dv = plan.debug_views(i)
+            st.W.append(None)
+            st.dW.append(Wd[i].double().cpu().numpy() - before[k])
+            st.M.append(M.double().cpu().numpy())
+            st.l.append(l.double().cpu().numpy())
+            st.r.append(r.double().cpu().numpy())
+            st.nu.append(float(nu.item()) if nu is not None else None)
+            st.Lv.append(dv["Lv"].double().cpu().numpy())
+            st.Rv.append(dv["Rv"].double().cpu().numpy())
+            st.O.append(dv["O"].float().double().cpu().numpy())
+            st.X0.append(None)
+            st.scal.append({k2: float(v.item()) for k2, v in dv["scalars"].items()})
+        del before
+        Wo, inter = oracle_step(Wo, [gh[i] for i in sample], ost, ohp)
+        orc = {"inter": inter, "M": ost.M, "l": ost.l, "r": ost.r, "nu": list(ost.nu)}
+        w_t = compare([st], [orc], w.variant, tol_ns=tol_ns, tol_state=tol_state, label=f"{label} step {t}")
+        for k2, v in w_t.items():
+            worst[k2] = max(worst.get(k2, 0.0), v)
+        say(f"[parity] {label} step {t}: dW {w_t['dW']:.3e} O {w_t['O']:.3e} M {w_t['M']:.3e}")
+        del st, inter, orc
+    plan.close()
+    return worst
+
+
 def run_oracle(shapes, variant: str, W0, grads, hp_kw: dict, collect=None):
     """The same steps through the oracle, restricted to the matrices in `collect`."""
     idx = list(range(len(shapes))) if collect is None else list(collect)

@@ -6,7 +6,8 @@ same float32 buffers.  Each test prints its case before touching the GPU.
 import numpy as np
 import pytest
 
-from gpu_harness import TOL_NS, TOL_STATE, compare, run_gpu, run_oracle, say, to_dev
+from gpu_harness import (TOL_NS, TOL_STATE, compare, run_gpu, run_oracle, run_sampled_against_oracle, say,
+                         to_dev)
 from oracle import rel_fro
 from paper_2608_05088_amd import libmalt as lm
 from paper_2608_05088_amd import workloads as wl
@@ -277,6 +278,46 @@ def test_c4_gpt2_large_sampled():
     o = run_oracle(list(w.shapes), w.variant, W0, grads, _hp(w), collect=sample)
     worst = compare(g, o, w.variant, label="C4")
     say(f"[parity] C4 worst {worst}")
+
+
+@pytest.mark.slow
+def test_c4_gpt2_large_ten_steps_persistent_state():
+    # The benchmark's timed configuration: ten consecutive steps of the full
+    # 144-matrix plan with persistent state and fresh gradients per step; the
+    # oracle follows eight matrices (one of each shape from the first and last
+    # blocks) through all ten steps and every step is compared.
+    w = wl.WORKLOADS[4]
+    sample = [0, 1, 2, 3, 140, 141, 142, 143]
+    say(f"[parity] C4 gpt2-large {len(w.shapes)} matrices {w.variant} x{w.steps}, oracle on {sample}")
+    worst = run_sampled_against_oracle(w, w.steps, sample, _hp(w), label="C4x10")
+    say(f"[parity] C4 x{w.steps} worst {worst}")
+
+
+@pytest.mark.slow
+def test_c5_stress_full_plan_one_step():
+    # C5 as configured: one MALTER step over all 128 matrices in one grouped
+    # plan (its own XCD-balanced tile lists); four matrices, two of each
+    # shape from both ends of the list, are compared with the oracle.
+    w = wl.WORKLOADS[5]
+    sample = [0, 1, 126, 127]
+    say(f"[parity] C5 stress {len(w.shapes)} matrices {w.variant} x1, oracle on {sample}")
+    worst = run_sampled_against_oracle(w, 1, sample, _hp(w), label="C5 full")
+    say(f"[parity] C5 full plan worst {worst}")
+
+
+@pytest.mark.parametrize("ns_steps", [2, 4])
+def test_even_newton_schulz_step_counts(ns_steps):
+    # With an even iteration count the final O lands in the first X buffer
+    # (the odd counts of every other test end in the second).
+    shapes = [(768, 2304), (2304, 768), (100, 900), (20, 300)]
+    say(f"[parity] ns_steps={ns_steps} {shapes} malter x2")
+    W0 = [wl.weight(88, i, s) for i, s in enumerate(shapes)]
+    grads = [[wl.grad(88, t, i, s, "row_loguniform") for i, s in enumerate(shapes)] for t in (1, 2)]
+    hp = dict(lr=5e-3, ns_steps=ns_steps)
+    g = run_gpu(shapes, "malter", W0, grads, hp)
+    o = run_oracle(shapes, "malter", W0, grads, hp)
+    worst = compare(g, o, "malter", label=f"ns{ns_steps}")
+    say(f"[parity] ns_steps={ns_steps} worst {worst}")
 
 
 @pytest.mark.slow
