@@ -32,7 +32,8 @@
  *    rounded up to multiples of 256.  Device pointers must be 4-byte aligned; rows whose
  *    start is 16-byte aligned with cols % 4 == 0 take a vectorised path.
  *  - All device memory is owned by the caller.  The library never allocates
- *    device or pinned host memory.
+ *    device or pinned host memory; malt_init_state_scratch plans use the
+ *    library's static scratch array instead of a caller workspace.
  *  - `stream` is a hipStream_t (NULL = the legacy default stream).  Steps are
  *    enqueued asynchronously; argument errors are detected on the host before
  *    anything is enqueued and leave the state untouched.
@@ -59,7 +60,8 @@ typedef enum {
   MALT_ERR_ALIGNMENT = 3,       /* a device pointer is not 4-byte aligned             */
   MALT_ERR_STATE_MISMATCH = 4,  /* shapes or variant differ from those given at init  */
   MALT_ERR_HIP = 5,             /* a HIP runtime call failed                          */
-  MALT_ERR_ALIAS = 6            /* params / grads / state / workspace overlap          */
+  MALT_ERR_ALIAS = 6,           /* params / grads / state / workspace overlap          */
+  MALT_ERR_SCRATCH_SIZE = 7     /* workspace larger than the static scratch array      */
 } malt_status_t;
 
 typedef enum { MALT_VARIANT_MALT = 0, MALT_VARIANT_MALTER = 1 } malt_variant_t;
@@ -124,6 +126,28 @@ malt_status_t malt_state_size(const malt_shape_t* shapes, int32_t n, malt_varian
 malt_status_t malt_init_state(malt_plan_t** out, const malt_shape_t* shapes, int32_t n,
                               malt_variant_t variant, void* state_mem, void* workspace_mem,
                               int32_t from_existing, int64_t step, void* stream);
+
+/* Bytes of the library's static device scratch array (64 MiB). */
+#define MALT_SCRATCH_BYTES (64ull << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same as
+ * malt_init_state, but the workspace is a static array inside the library
+ * (MALT_SCRATCH_BYTES per device, held until the process ends) instead of a
+ * caller buffer.  Neither this call nor the steps of its plan call hipMalloc,
+ * hipFree or any other allocating routine; the caller still allocates the
+ * state and the parameters and gradients.
+ * Errors: MALT_ERR_SCRATCH_SIZE when malt_state_size's workspace_bytes for these
+ * shapes exceeds MALT_SCRATCH_BYTES (nothing is enqueued), plus those of
+ * malt_init_state.
+ * Sharing: every scratch plan on a device uses that device's one array.
+ * Creating a scratch plan takes the array over (it zeroes it and writes its
+ * tables there); steps of an older scratch plan on the same device then fail
+ * with MALT_ERR_STATE_MISMATCH.  Work of two scratch plans that overlaps in
+ * time on one device races on the array. */
+malt_status_t malt_init_state_scratch(malt_plan_t** out, const malt_shape_t* shapes, int32_t n,
+                                      malt_variant_t variant, void* state_mem, int32_t from_existing,
+                                      int64_t step, void* stream);
 
 /* Enqueue one step (Algorithm 1 or 2 by the plan's variant) on `stream`.
  * params[i]: device float32 rows x cols, updated in place.

@@ -8,6 +8,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -313,6 +314,47 @@ bool ranges_overlap(uintptr_t a0, size_t an, uintptr_t b0, size_t bn) {
 
 }  // namespace
 
+// The workspace of plans made by malt_init_state_scratch, for callers that
+// cannot allocate device memory.  Every device the library runs on holds its
+// own copy until the process ends.  In host code `scratch` names a host-side
+// stand-in: the device address comes from hipGetSymbolAddress, fetched once per
+// device (with that device current) and kept in g_scratch_ptr.
+static __device__ __align__(256) unsigned char scratch[MALT_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch_ptr[kMaxDevices] = {};
+uint64_t g_scratch_gen[kMaxDevices] = {};
+
+// The current device's scratch address and a new generation for it: a plan
+// holding an older generation has lost the array to the newer plan.
+malt_status_t scratch_claim(int* dev, char** ptr, uint64_t* gen) {
+  hipError_t e = hipGetDevice(dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (*dev < 0 || *dev >= kMaxDevices) return fail(MALT_ERR_INVALID_ARG, "device %d out of range", *dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[*dev]) {
+    void* a = nullptr;
+    e = hipGetSymbolAddress(&a, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!a || reinterpret_cast<uintptr_t>(a) % 256 != 0)
+      return fail(MALT_ERR_HIP, "static scratch array has no usable device address");
+    g_scratch_ptr[*dev] = static_cast<char*>(a);
+  }
+  *ptr = g_scratch_ptr[*dev];
+  *gen = ++g_scratch_gen[*dev];
+  return MALT_OK;
+}
+
+bool scratch_current(int dev, uint64_t gen) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  return dev >= 0 && dev < kMaxDevices && g_scratch_gen[dev] == gen;
+}
+
+}  // namespace
+
 struct malt_plan {
   Layout L;
   malt_variant_t variant;
@@ -324,6 +366,11 @@ struct malt_plan {
   // pointer table last written to the workspace (compared on every step)
   std::vector<PtrPair> cur_ptrs;
   bool ptrs_valid = false;
+  // workspace in the library's static scratch array of device `device`,
+  // valid while that device's scratch generation still equals scratch_gen
+  bool scratch = false;
+  int device = -1;
+  uint64_t scratch_gen = 0;
   // profiling
   bool prof = false;
   struct EvSet { std::vector<hipEvent_t> ev; std::vector<int> phase; };
@@ -530,6 +577,34 @@ malt_status_t malt_init_state(malt_plan_t** out, const malt_shape_t* shapes, int
   return MALT_OK;
 }
 
+malt_status_t malt_init_state_scratch(malt_plan_t** out, const malt_shape_t* shapes, int32_t n,
+                                      malt_variant_t variant, void* state_mem, int32_t from_existing,
+                                      int64_t step, void* stream) {
+  if (!out) return fail(MALT_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  malt_status_t st = check_init_args(shapes, n, variant, state_mem, from_existing, step);
+  if (st != MALT_OK) return st;
+  Layout L = make_layout(shapes, n, variant);
+  if (L.ws_bytes > MALT_SCRATCH_BYTES)
+    return fail(MALT_ERR_SCRATCH_SIZE, "these shapes need a %zu-byte workspace; the static scratch holds %llu bytes "
+                "(use malt_init_state with a caller-allocated workspace)", L.ws_bytes,
+                (unsigned long long)MALT_SCRATCH_BYTES);
+  int dev = -1;
+  char* ws = nullptr;
+  uint64_t gen = 0;
+  st = scratch_claim(&dev, &ws, &gen);
+  if (st != MALT_OK) return st;
+  malt_plan* p = new malt_plan();
+  p->L = std::move(L);
+  p->scratch = true;
+  p->device = dev;
+  p->scratch_gen = gen;
+  st = init_plan(p, shapes, n, variant, state_mem, ws, from_existing, step, stream);
+  if (st != MALT_OK) { delete p; return st; }
+  *out = p;
+  return MALT_OK;
+}
+
 malt_status_t malt_step(malt_plan_t* p, float* const* params, const float* const* grads,
                         const malt_shape_t* shapes, int32_t n, const malt_hparams_t* hp, void* stream) {
   if (!p) return fail(MALT_ERR_INVALID_ARG, "plan is NULL");
@@ -566,6 +641,10 @@ malt_status_t malt_step(malt_plan_t* p, float* const* params, const float* const
       if (rs[i - 1].first + rs[i - 1].second > rs[i].first)
         return fail(MALT_ERR_ALIAS, "two parameter matrices overlap");
   }
+
+  if (p->scratch && !scratch_current(p->device, p->scratch_gen))
+    return fail(MALT_ERR_STATE_MISMATCH, "the static scratch of device %d now belongs to a newer plan; "
+                "this plan's workspace is gone", p->device);
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   hipError_t e;
@@ -777,6 +856,7 @@ const char* malt_status_string(malt_status_t s) {
     case MALT_ERR_STATE_MISMATCH: return "MALT_ERR_STATE_MISMATCH";
     case MALT_ERR_HIP: return "MALT_ERR_HIP";
     case MALT_ERR_ALIAS: return "MALT_ERR_ALIAS";
+    case MALT_ERR_SCRATCH_SIZE: return "MALT_ERR_SCRATCH_SIZE";
   }
   return "MALT_ERR_UNKNOWN";
 }

@@ -22,6 +22,8 @@ MALT_ERR_ALIGNMENT = 3
 MALT_ERR_STATE_MISMATCH = 4
 MALT_ERR_HIP = 5
 MALT_ERR_ALIAS = 6
+MALT_ERR_SCRATCH_SIZE = 7
+MALT_SCRATCH_BYTES = 64 << 20
 
 MALT_VARIANT_MALT = 0
 MALT_VARIANT_MALTER = 1
@@ -76,6 +78,8 @@ _SIGNATURES = [
                                   POINTER(c_size_t)]),
     ("malt_init_state", c_int32, [POINTER(c_void_p), POINTER(malt_shape_t), c_int32, c_int32,
                                   c_void_p, c_void_p, c_int32, c_int64, c_void_p]),
+    ("malt_init_state_scratch", c_int32, [POINTER(c_void_p), POINTER(malt_shape_t), c_int32, c_int32,
+                                          c_void_p, c_int32, c_int64, c_void_p]),
     ("malt_step", c_int32, [c_void_p, POINTER(c_void_p), POINTER(c_void_p), POINTER(malt_shape_t),
                             c_int32, POINTER(malt_hparams_t), c_void_p]),
     ("malt_state_layout", c_int32, [c_void_p, c_int32, POINTER(malt_state_layout_t)]),
@@ -160,10 +164,15 @@ def _stream_handle(stream) -> Optional[int]:
 
 
 class Plan:
-    """A libmalt plan over torch-allocated state and workspace buffers."""
+    """A libmalt plan over torch-allocated state and workspace buffers.
+
+    scratch=True builds the plan with malt_init_state_scratch: no workspace
+    tensor is allocated, the library's static per-device scratch array serves
+    instead (debug_views are then unavailable)."""
 
     def __init__(self, shapes: Sequence[Tuple[int, int]], variant: str = "malt", device=None,
-                 stream=None, state=None, from_existing: bool = False, step: int = 0):
+                 stream=None, state=None, from_existing: bool = False, step: int = 0,
+                 scratch: bool = False):
         import torch
         self.shapes: List[Tuple[int, int]] = [(int(m), int(n)) for m, n in shapes]
         self.variant = variant
@@ -178,14 +187,22 @@ class Plan:
         elif state.numel() * state.element_size() < sb:
             raise ValueError("state buffer too small")
         self.state = state
-        self.workspace = torch.empty(wb, dtype=torch.uint8, device=self.device)
+        self.scratch = bool(scratch)
         self._c_shapes = _shapes(self.shapes)
         handle = c_void_p()
         with torch.cuda.device(self.device):   # the plan's device is current during set-up
-            _check(lib().malt_init_state(ctypes.byref(handle), self._c_shapes, len(self.shapes),
-                                         VARIANTS[variant], c_void_p(self.state.data_ptr()),
-                                         c_void_p(self.workspace.data_ptr()), int(from_existing),
-                                         int(step), c_void_p(_stream_handle(stream))))
+            if self.scratch:
+                self.workspace = None
+                _check(lib().malt_init_state_scratch(ctypes.byref(handle), self._c_shapes, len(self.shapes),
+                                                     VARIANTS[variant], c_void_p(self.state.data_ptr()),
+                                                     int(from_existing), int(step),
+                                                     c_void_p(_stream_handle(stream))))
+            else:
+                self.workspace = torch.empty(wb, dtype=torch.uint8, device=self.device)
+                _check(lib().malt_init_state(ctypes.byref(handle), self._c_shapes, len(self.shapes),
+                                             VARIANTS[variant], c_void_p(self.state.data_ptr()),
+                                             c_void_p(self.workspace.data_ptr()), int(from_existing),
+                                             int(step), c_void_p(_stream_handle(stream))))
         self._h = handle
 
     # -- stepping ----------------------------------------------------------------
@@ -245,6 +262,8 @@ class Plan:
     def debug_views(self, i: int) -> dict:
         """Torch views of matrix i's last-step intermediates in the workspace."""
         import torch
+        if self.workspace is None:
+            raise RuntimeError("debug_views need a caller workspace (this plan uses the static scratch)")
         L = self.debug_layout(i)
         m, n = self.shapes[i]
         w = self.workspace

@@ -113,6 +113,22 @@ def test_init_rejects_bad_pointers_before_device_work(L):
     assert out.value is None
 
 
+def test_scratch_init_rejects_before_device_work(L):
+    # The static scratch holds MALT_SCRATCH_BYTES; larger workspaces, NULL or
+    # misaligned state are refused on the host.
+    out = c_void_p()
+    big = lm._shapes([(4096, 4096)])
+    assert lm.malt_state_size([(4096, 4096)])[1] > lm.MALT_SCRATCH_BYTES
+    assert L.malt_init_state_scratch(ctypes.byref(out), big, 1, 0, c_void_p(0x10000), 0, 0, None) == lm.MALT_ERR_SCRATCH_SIZE
+    assert "static scratch" in lm.last_error()
+    small = lm._shapes([(8, 8)])
+    assert L.malt_init_state_scratch(ctypes.byref(out), small, 1, 0, None, 0, 0, None) == lm.MALT_ERR_INVALID_ARG
+    assert L.malt_init_state_scratch(ctypes.byref(out), small, 1, 0, c_void_p(0x10004), 0, 0, None) == lm.MALT_ERR_ALIGNMENT
+    assert L.malt_init_state_scratch(None, small, 1, 0, c_void_p(0x10000), 0, 0, None) == lm.MALT_ERR_INVALID_ARG
+    assert lm.status_string(lm.MALT_ERR_SCRATCH_SIZE) == "MALT_ERR_SCRATCH_SIZE"
+    assert out.value is None
+
+
 def test_step_rejects_null_plan_and_bad_hparams(L):
     shapes = lm._shapes([(8, 8)])
     P = (c_void_p * 1)(c_void_p(0x1000))
