@@ -26,8 +26,8 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0    # MI355X dense bf16 matrix-core peak
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "ns_update_gpt2_large_traffic.md")
-# The update kernel is built from ns_gemm.hip with the stage geometry ns_update.hip sets.
-NS_SOURCES = [os.path.join(ROOT, "paper_2608_05088_amd", "csrc", f) for f in ("ns_gemm.hip", "ns_update.hip")]
+# Sources of the update kernel (its shared pipeline header, then the kernel).
+NS_SOURCES = [os.path.join(ROOT, "paper_2608_05088_amd", "csrc", f) for f in ("ns_common.h", "ns_update.hip")]
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
 METRIC = "MALT step latency (ms) per GPT-2 param set; NS MFMA % bf16 peak; HBM GB/s"
 

@@ -61,7 +61,8 @@ typedef enum {
   MALT_ERR_STATE_MISMATCH = 4,  /* shapes or variant differ from those given at init  */
   MALT_ERR_HIP = 5,             /* a HIP runtime call failed                          */
   MALT_ERR_ALIAS = 6,           /* params / grads / state / workspace overlap          */
-  MALT_ERR_SCRATCH_SIZE = 7     /* workspace larger than the static scratch array      */
+  MALT_ERR_SCRATCH_SIZE = 7,    /* workspace larger than the static scratch array      */
+  MALT_ERR_BOUNDS = 8           /* malt_check_bounds found an address range outside its buffer */
 } malt_status_t;
 
 typedef enum { MALT_VARIANT_MALT = 0, MALT_VARIANT_MALTER = 1 } malt_variant_t;
@@ -192,6 +193,26 @@ typedef struct {
   int64_t A, B, AB_pitch, B_split;
 } malt_debug_layout_t;
 malt_status_t malt_debug_layout(const malt_plan_t* plan, int32_t i, malt_debug_layout_t* out);
+
+/* Host-side proof that the kernels of a plan over these shapes stay inside
+ * their buffers; for tests and for callers who want the check for their own
+ * shapes.  Needs no plan and no device: it builds the work lists that
+ * malt_init_state would build and, for every entry of every list (padding
+ * entries of the XCD-ordered Newton-Schulz lists included), derives with the
+ * kernels' own address functions the byte ranges the kernel can address: the
+ * direct-load spans of both operands over the whole contraction, stores of
+ * output tiles and mirrors, partial-slot indices, the layout of the workspace
+ * regions.  The Newton-Schulz operand offsets, passed to the hardware as
+ * 32-bit buffer offsets, must also stay below 4 GiB.
+ * shrink_bytes >= 0 checks the Newton-Schulz operand and output buffers (the
+ * ones read through buffer resources with the hardware range check off) as if
+ * they were that many bytes shorter: with 16 it must fail, since the kernels
+ * reach the last bytes of those buffers.
+ * Returns MALT_OK with *ranges_checked = the number of checks made, or
+ * MALT_ERR_BOUNDS with malt_last_error() naming the first kernel, matrix,
+ * tile and byte range that does not fit (or the usual argument errors). */
+malt_status_t malt_check_bounds(const malt_shape_t* shapes, int32_t n, malt_variant_t variant,
+                                int64_t shrink_bytes, int64_t* ranges_checked);
 
 /* Step counter t (number of steps enqueued so far). */
 int64_t malt_plan_step(const malt_plan_t* plan);

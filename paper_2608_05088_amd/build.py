@@ -13,7 +13,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "lib", "libmalt.so")
-SOURCES = ["malt_api.hip", "elementwise.hip", "ns_gemm.hip", "ns_update.hip", "small_ns.hip"]
+SOURCES = ["malt_api.hip", "elementwise.hip", "ns_sym.hip", "ns_update.hip", "small_ns.hip"]
 ARCH = "gfx950"
 
 

@@ -225,17 +225,26 @@ __global__ __launch_bounds__(K2W_THREADS) void scale_convert_wide_kernel(EwArgs 
 // transpose. Tiles cover W-oriented padded rows x cols in K2_T x K2_T blocks;
 // one workgroup converts K2_GROUP consecutive tiles, a 64-row band of
 // K2_GROUP * 64 W columns of one matrix (a matrix's tiles are listed band by
-// band, and every band holds a multiple of K2_GROUP tiles). All loads of the
-// band are issued before any conversion.
+// band, and every band holds a multiple of K2_GROUP tiles).
+// Each thread converts two consecutive W rows of four W columns per tile, so
+// it holds, per W column, the two bf16 values of one 32-bit word of the
+// canonical row (canonical columns 2p, 2p + 1).  The words go to LDS as
+// [canonical row][word] with a pitch of 33 words: the 64 lanes of a write
+// (16 column groups x 4 row pairs) hit 64 distinct banks.  The copy-out reads
+// 16-byte row pieces back as four words (at most 2-way bank conflicts) and
+// stores 128-byte row pieces of X0.
 template <bool MALTER>
 __global__ __launch_bounds__(K2T_THREADS) void scale_convert_tall_kernel(EwArgs a) {
   constexpr int TG = K2_GROUP;
   constexpr int NW = K2T_THREADS / 64;
-  constexpr int RQ = K2T_THREADS / 16;   // row groups: 16 threads x 4 columns span a tile's 64 columns
-  constexpr int P = K2_T / RQ;           // rows per thread and tile
-  constexpr int SEGS = K2T_THREADS / K2_T, SEG = K2_T / SEGS;   // transposed write: W rows per thread
-  static_assert(P * RQ == K2_T && SEGS * SEG == K2_T && SEG % 8 == 0, "tall tile layout");
-  __shared__ bf16_t tsh[TG][K2_T][K2_T + 2];
+  constexpr int NP = K2T_THREADS / 16;         // row pairs per pass: 16 threads x 4 columns span 64 columns
+  constexpr int PASSES = K2_T / (2 * NP);      // row-pair passes per tile
+  constexpr int WPR = K2_T / 2;                // words per canonical row of a tile
+  constexpr int PITCH = WPR + 1;               // LDS words per staged canonical row
+  constexpr int CPR = WPR / 4;                 // 16-byte pieces per canonical row of a tile
+  constexpr int ROWS_OUT = K2T_THREADS / CPR;  // canonical rows per copy-out pass
+  static_assert(PASSES * 2 * NP == K2_T && K2_T % ROWS_OUT == 0, "tall tile layout");
+  __shared__ uint32_t tsh[TG][K2_T][PITCH];
   __shared__ float red[2 * TG][NW];
   const int grp = xcd_remap(blockIdx.x, gridDim.x);
   const Tile t = a.tiles[grp * TG];
@@ -247,37 +256,41 @@ __global__ __launch_bounds__(K2T_THREADS) void scale_convert_tall_kernel(EwArgs 
   const MALT_GLOBAL float* __restrict__ M = gptr(d.M);
   const MALT_GLOBAL float* __restrict__ G = gptr(a.ptrs[t.mat].G);
   const int r0 = t.ti * K2_T, cb = t.tj * K2_T;   // band columns cb .. cb + TG*K2_T
-  const int cc = (threadIdx.x & 15) * 4;          // 4 columns of each tile
-  const int rq = threadIdx.x >> 4;                // rows rq + RQ p, p < P
+  const int cg = threadIdx.x & 15;                // W columns 4 cg .. 4 cg + 3 of each tile
+  const int pp = threadIdx.x >> 4;                // row pair pp + NP * pass
 
-  float Li[P];
+  float Li[PASSES][2];
 #pragma unroll
-  for (int p = 0; p < P; ++p) {
-    const int r = r0 + p * RQ + rq;
-    Li[p] = r < m ? gptr(d.Lv)[r] : 0.f;
-  }
+  for (int ps = 0; ps < PASSES; ++ps)
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int r = r0 + 2 * (pp + NP * ps) + u;
+      Li[ps][u] = r < m ? gptr(d.Lv)[r] : 0.f;
+    }
   float Rv[TG][4];
 #pragma unroll
   for (int j = 0; j < TG; ++j)
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const int c = cb + j * K2_T + cc + e;
+      const int c = cb + j * K2_T + 4 * cg + e;
       Rv[j][e] = c < n ? gptr(d.Rv)[c] : 0.f;
     }
-  float mm[TG][P][4], gg[TG][P][4];
+  float mm[TG][PASSES][2][4], gg[TG][PASSES][2][4];
 #pragma unroll
   for (int j = 0; j < TG; ++j)
 #pragma unroll
-    for (int p = 0; p < P; ++p) {
-      const int r = r0 + p * RQ + rq;
-      const int c = cb + j * K2_T + cc;
+    for (int ps = 0; ps < PASSES; ++ps)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) mm[j][p][e] = gg[j][p][e] = 0.f;
-      if (r < m) {
-        load4(M + (size_t)r * n, c, n, vec, mm[j][p]);
-        if (MALTER) load4(G + (size_t)r * n, c, n, vec, gg[j][p]);
+      for (int u = 0; u < 2; ++u) {
+        const int r = r0 + 2 * (pp + NP * ps) + u;
+        const int c = cb + j * K2_T + 4 * cg;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) mm[j][ps][u][e] = gg[j][ps][u][e] = 0.f;
+        if (r < m) {
+          load4(M + (size_t)r * n, c, n, vec, mm[j][ps][u]);
+          if (MALTER) load4(G + (size_t)r * n, c, n, vec, gg[j][ps][u]);
+        }
       }
-    }
 
   float s2[TG], q2[TG];
 #pragma unroll
@@ -285,44 +298,36 @@ __global__ __launch_bounds__(K2T_THREADS) void scale_convert_tall_kernel(EwArgs 
     s2[j] = 0.f;
     q2[j] = 0.f;
 #pragma unroll
-    for (int p = 0; p < P; ++p) {
-      const int rr = p * RQ + rq;
-      float x[4];
+    for (int ps = 0; ps < PASSES; ++ps) {
+      const int p = pp + NP * ps;   // word index: W rows 2p, 2p + 1 of the tile
+      float x[2][4];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        x[e] = Li[p] * mm[j][p][e] * Rv[j][e];
-        s2[j] += x[e] * x[e];
-        if (MALTER) {
-          const float y = Li[p] * gg[j][p][e] * Rv[j][e];
-          q2[j] += y * y;
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          x[u][e] = Li[ps][u] * mm[j][ps][u][e] * Rv[j][e];
+          s2[j] += x[u][e] * x[u][e];
+          if (MALTER) {
+            const float y = Li[ps][u] * gg[j][ps][u][e] * Rv[j][e];
+            q2[j] += y * y;
+          }
         }
-      }
-      const uint32_t lo = pack_bf16x2(x[0], x[1]), hi = pack_bf16x2(x[2], x[3]);
-      tsh[j][rr][cc + 0] = (bf16_t)(lo & 0xffffu);
-      tsh[j][rr][cc + 1] = (bf16_t)(lo >> 16);
-      tsh[j][rr][cc + 2] = (bf16_t)(hi & 0xffffu);
-      tsh[j][rr][cc + 3] = (bf16_t)(hi >> 16);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) tsh[j][4 * cg + e][p] = pack_bf16x2(x[0][e], x[1][e]);
     }
   }
   __syncthreads();
-  // Transposed write: thread -> (W column ct, SEG-row segment) of each tile.
-  const int ct = threadIdx.x / SEGS;
-  const int seg = (threadIdx.x % SEGS) * SEG;
+  // Copy-out: thread -> (canonical row, 16-byte piece); CPR threads per row.
+  const int piece = threadIdx.x % CPR;
 #pragma unroll
-  for (int j = 0; j < TG; ++j) {
-    MALT_GLOBAL ew_u32x4* dst = reinterpret_cast<MALT_GLOBAL ew_u32x4*>(X0 + (size_t)(cb + j * K2_T + ct) * ldx + r0 + seg);
+  for (int j = 0; j < TG; ++j)
 #pragma unroll
-    for (int h = 0; h < SEG / 8; ++h) {
-      uint32_t wv[4];
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int rr = seg + 8 * h + 2 * k;
-        wv[k] = (uint32_t)tsh[j][rr][ct] | ((uint32_t)tsh[j][rr + 1][ct] << 16);
-      }
-      const ew_u32x4 v = {wv[0], wv[1], wv[2], wv[3]};
-      __builtin_nontemporal_store(v, dst + h);
+    for (int rr = threadIdx.x / CPR; rr < K2_T; rr += ROWS_OUT) {
+      const uint32_t* src = &tsh[j][rr][4 * piece];
+      const ew_u32x4 v = {src[0], src[1], src[2], src[3]};
+      __builtin_nontemporal_store(
+          v, reinterpret_cast<MALT_GLOBAL ew_u32x4*>(X0 + (size_t)(cb + j * K2_T + rr) * ldx + r0 + 8 * piece));
     }
-  }
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
 #pragma unroll
   for (int j = 0; j < TG; ++j) {
@@ -410,10 +415,23 @@ __global__ __launch_bounds__(NTHREADS) void graft_scalars_kernel(EwArgs a) {
 // W^T for tall ones (read through an LDS transpose).  Reads W and O, writes
 // W: 10 bytes per element.
 // ---------------------------------------------------------------------------
+// Tall matrices: the tile's O^T block (EW_TC canonical rows = W columns, EW_TR
+// canonical columns = W rows) is staged in LDS as 32-bit words, word w holding
+// W rows 2w and 2w + 1 of one W column.  bm_word() places word (c, w), with
+// c = 4 l + e, in a 64-word segment per (w, e) that holds the 64 values of l
+// rotated by 16 e + 4 (w / 4).  The fill (each thread: 16 bytes of one
+// canonical row, four words) and the read (a wave's two W rows are one word;
+// lane l reads W columns 4 l .. 4 l + 3) both hit 64 distinct banks.
+__device__ __forceinline__ int bm_word(int c, int w) {
+  const int l = c >> 2, e = c & 3;
+  return w * EW_TC + e * 64 + ((l + 16 * e + 4 * (w >> 2)) & 63);
+}
+
 __global__ __launch_bounds__(EW_THREADS) void backmap_write_kernel(EwArgs a) {
   constexpr int NW = EW_THREADS / 64, RPW = EW_TR / NW;   // 16 waves, 2 rows each
   static_assert(NW * RPW == EW_TR && EW_TC * EW_TR == EW_THREADS * 8, "tall fill: 8 bf16 per thread");
-  __shared__ bf16_t osh[EW_TC][EW_TR + 2];   // tall: O^T block, [W col][W row]
+  static_assert(RPW == 2 && EW_TC == 256, "tall read: one word holds a wave's two rows; 64 lanes x 4 columns");
+  __shared__ uint32_t osh[EW_TR / 2 * EW_TC];   // tall: O^T block as words (see bm_word)
   const Tile t = a.tiles[xcd_remap(blockIdx.x, gridDim.x)];
   const MatDesc& d = a.desc[t.mat];
   const int m = d.m, n = d.n;
@@ -427,16 +445,15 @@ __global__ __launch_bounds__(EW_THREADS) void backmap_write_kernel(EwArgs a) {
   const float decay = a.decay;
   if (d.tall) {
     // Canonical rows c0 .. c0+255 (W columns), columns r0 .. r0+31 (W rows):
-    // four threads per canonical row, 16 bytes each (inside the padded buffer).
+    // four threads per canonical row, 16 bytes (four words) each, inside the
+    // padded buffer.
     const int cr = threadIdx.x >> 2, q = threadIdx.x & 3;
     const ew_u32x4 v =
         __builtin_nontemporal_load(reinterpret_cast<const MALT_GLOBAL ew_u32x4*>(O + (size_t)(c0 + cr) * ldo + r0 + q * 8));
-    const uint32_t vw[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      osh[cr][q * 8 + 2 * k] = (bf16_t)(vw[k] & 0xffffu);
-      osh[cr][q * 8 + 2 * k + 1] = (bf16_t)(vw[k] >> 16);
-    }
+    osh[bm_word(cr, 4 * q + 0)] = v.x;
+    osh[bm_word(cr, 4 * q + 1)] = v.y;
+    osh[bm_word(cr, 4 * q + 2)] = v.z;
+    osh[bm_word(cr, 4 * q + 3)] = v.w;
     __syncthreads();
   }
   float Rv[4];
@@ -454,6 +471,11 @@ __global__ __launch_bounds__(EW_THREADS) void backmap_write_kernel(EwArgs a) {
       }
     }
   }
+  uint32_t ow[4];   // tall: W rows rw, rw + 1 at W column c + e
+  if (d.tall) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) ow[e] = osh[bm_word(4 * lane + e, w)];
+  }
 #pragma unroll
   for (int u = 0; u < RPW; ++u) {
     const int r = rw + u;
@@ -461,13 +483,13 @@ __global__ __launch_bounds__(EW_THREADS) void backmap_write_kernel(EwArgs a) {
     const float cl = coef * gptr(d.Lv)[r];
     float o[4];
     if (!d.tall) {
-      o[0] = bf2f((bf16_t)(pk[u].x & 0xffffu));
-      o[1] = bf2f((bf16_t)(pk[u].x >> 16));
-      o[2] = bf2f((bf16_t)(pk[u].y & 0xffffu));
-      o[3] = bf2f((bf16_t)(pk[u].y >> 16));
+      o[0] = bf16_lo(pk[u].x);
+      o[1] = bf16_hi(pk[u].x);
+      o[2] = bf16_lo(pk[u].y);
+      o[3] = bf16_hi(pk[u].y);
     } else {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) o[e] = bf2f(osh[lane * 4 + e][w * RPW + u]);
+      for (int e = 0; e < 4; ++e) o[e] = u == 0 ? bf16_lo(ow[e]) : bf16_hi(ow[e]);
     }
 #pragma unroll
     for (int e = 0; e < 4; ++e) wv[u][e] = decay * wv[u][e] - cl * o[e] * Rv[e];

@@ -14,6 +14,7 @@
 
 #include "../../include/libmalt.h"
 #include "malt_internal.h"
+#include "ns_common.h"
 
 using namespace malt;
 
@@ -527,6 +528,251 @@ malt_status_t init_plan(malt_plan* p, const malt_shape_t* shapes, int32_t n, mal
   return MALT_OK;
 }
 
+
+// ---------------------------------------------------------------------------
+// Host-side bounds check of the work lists (no device work).  For every entry
+// of every list it derives, with the kernels' own address functions where the
+// kernels compute offsets (ns_common.h), the byte ranges the kernel can touch
+// and checks them against the buffer each lies in.
+// ---------------------------------------------------------------------------
+struct BoundsCheck {
+  const Layout& L;
+  int64_t shrink = 0;
+  int64_t checked = 0;
+  malt_status_t st = MALT_OK;
+
+  // [lo, hi) inside a buffer of `size` bytes (minus shrink unless exact);
+  // off32: the range is addressed with 32-bit offsets from the buffer's base.
+  bool range(const char* kernel, const char* buf, const Tile& t, uint64_t lo, uint64_t hi, uint64_t size,
+             bool off32 = false, bool exact = false) {
+    ++checked;
+    const uint64_t lim = exact ? size : size > uint64_t(shrink) ? size - uint64_t(shrink) : 0;
+    if (lo <= hi && hi <= lim && (!off32 || hi <= (uint64_t(1) << 32))) return true;
+    st = fail(MALT_ERR_BOUNDS, "%s: matrix %d tile (%d, %d, %d): %s bytes [%llu, %llu) outside [0, %llu)%s", kernel,
+              t.mat, t.ti, t.tj, t.idx, buf, (unsigned long long)lo, (unsigned long long)hi,
+              (unsigned long long)lim, off32 && hi > (uint64_t(1) << 32) ? " or beyond 32-bit offsets" : "");
+    return false;
+  }
+  // The same for the elementwise kernels' buffers, which shrink leaves alone:
+  // it tests the Newton-Schulz buffers, read with hardware range checks off.
+  bool erange(const char* kernel, const char* buf, const Tile& t, uint64_t lo, uint64_t hi, uint64_t size) {
+    return range(kernel, buf, t, lo, hi, size, false, true);
+  }
+  bool cond(bool ok, const char* kernel, const Tile& t, const char* what) {
+    ++checked;
+    if (ok) return true;
+    st = fail(MALT_ERR_BOUNDS, "%s: entry (mat %d, %d, %d, %d): %s", kernel, t.mat, t.ti, t.tj, t.idx, what);
+    return false;
+  }
+  bool mat_ok(const char* kernel, const Tile& t) {
+    return cond(t.mat >= 0 && size_t(t.mat) < L.mats.size(), kernel, t, "matrix index out of range");
+  }
+};
+
+malt_status_t check_bounds(const Layout& L, int64_t shrink, int64_t* checked) {
+  using SL = ns::SymLoads<ns::SymGeom>;
+  using UL = ns::UpdLoads<ns::UpdGeom>;
+  constexpr int NW = ns::NW, LANES = 64;
+  BoundsCheck B{L, shrink};
+  std::vector<Tile> ew, fin, k2, sym, upd, smg, smp, smu, gram, poly, updd;
+  build_tiles(L, ew, fin, k2, sym, upd, smg, smp, smu);
+  ns_dispatch_lists(L, sym, upd, gram, poly, updd);
+  const uint64_t u2 = 2, u4 = 4;
+
+  // Workspace regions lie inside the workspace, in order, without overlap.
+  {
+    const Tile none{-1, 0, 0, 0};
+    uint64_t end = L.ws_t_smu + sizeof(Tile) * smu.size();
+    for (const MatPlan& q : L.mats) {
+      const std::pair<size_t, uint64_t> regions[] = {
+          {q.ws_scal, 8 * MAT_SCALARS}, {q.ws_Lv, 4 * q.m}, {q.ws_Rv, 4 * q.n},
+          {q.ws_rowpart, 4 * uint64_t(q.k1_ct) * q.m}, {q.ws_colpart, 4 * uint64_t(q.k1_rt) * q.n},
+          {q.ws_k2part, 8 * uint64_t(q.k2_tiles)}, {q.ws_gpart, 8 * uint64_t(q.upd_tiles)},
+          {q.ws_X[0], 2 * uint64_t(q.mp) * q.np}, {q.ws_X[1], 2 * uint64_t(q.mp) * q.np},
+          {q.ws_A, 2 * uint64_t(q.mp) * q.mp}, {q.ws_B, 2 * uint64_t(q.mp) * q.mp * (q.split ? 2 : 1)}};
+      for (const auto& r : regions) {
+        if (!B.cond(r.first >= end, "layout", none, "workspace regions overlap")) return B.st;
+        end = r.first + r.second;
+      }
+      if (q.small) {
+        const std::pair<size_t, uint64_t> sm[] = {{q.ws_Xs[0], 4 * uint64_t(q.mc) * q.np},
+                                                  {q.ws_Xs[1], 4 * uint64_t(q.mc) * q.np},
+                                                  {q.ws_Ap, 4 * uint64_t(q.sm_gchunks) * NS_SMALL_MAX * NS_SMALL_MAX},
+                                                  {q.ws_Bs, 4 * uint64_t(NS_SMALL_MAX) * NS_SMALL_MAX}};
+        for (const auto& r : sm) {
+          if (!B.cond(r.first >= end, "layout", none, "workspace regions overlap")) return B.st;
+          end = r.first + r.second;
+        }
+      }
+    }
+    if (!B.range("layout", "workspace", none, 0, end, L.ws_bytes, false, true)) return B.st;
+  }
+
+  // Momentum (row / column partials) and back-map (W, G, M guarded by r < m
+  // and c < n in the kernels; O read inside the padded canonical buffer).
+  for (const Tile& t : ew) {
+    if (!B.mat_ok("momentum/back-map", t)) return B.st;
+    const MatPlan& q = L.mats[t.mat];
+    if (!B.cond(t.ti >= 0 && t.ti < q.k1_rt && t.tj >= 0 && t.tj < q.k1_ct, "momentum/back-map", t,
+                "tile outside the matrix's tile grid"))
+      return B.st;
+    const uint64_t r0 = uint64_t(t.ti) * EW_TR, c0 = uint64_t(t.tj) * EW_TC;
+    const uint64_t r1 = std::min<uint64_t>(r0 + EW_TR, q.m), c1 = std::min<uint64_t>(c0 + EW_TC, q.n);
+    if (!B.cond(r0 < uint64_t(q.m) && c0 < uint64_t(q.n), "momentum/back-map", t, "tile origin outside W")) return B.st;
+    if (!B.erange("momentum", "row partials", t, u4 * (t.tj * uint64_t(q.m) + r0), u4 * (t.tj * uint64_t(q.m) + r1),
+                 u4 * q.k1_ct * q.m) ||
+        !B.erange("momentum", "column partials", t, u4 * (t.ti * uint64_t(q.n) + c0),
+                 u4 * (t.ti * uint64_t(q.n) + c1), u4 * q.k1_rt * q.n))
+      return B.st;
+    const uint64_t osz = u2 * q.mp * q.np;
+    if (q.tall) {   // canonical rows c0 .. c0+255, columns r0 .. r0+31
+      if (!B.erange("back-map", "O (tall)", t, u2 * (c0 * q.np + r0), u2 * ((c0 + EW_TC - 1) * q.np + r0 + EW_TR), osz))
+        return B.st;
+    } else {        // rows r0 .. r1-1, columns c0 .. c0+255
+      if (!B.erange("back-map", "O (wide)", t, u2 * (r0 * q.np + c0), u2 * ((r1 - 1) * q.np + c0 + EW_TC), osz))
+        return B.st;
+    }
+  }
+  // Preconditioner finalise: chunks of FIN_W rows or columns.
+  for (const Tile& t : fin) {
+    if (!B.mat_ok("precond_finalize", t)) return B.st;
+    const MatPlan& q = L.mats[t.mat];
+    const int64_t len = t.ti == 0 ? q.m : q.n;
+    if (!B.cond((t.ti == 0 || t.ti == 1) && t.tj >= 0 && int64_t(t.tj) * FIN_W < len, "precond_finalize", t,
+                "chunk outside the rows / columns"))
+      return B.st;
+  }
+  // Scale+convert: X0 over the padded canonical domain; norm partial slots.
+  for (size_t k = 0; k < k2.size(); ++k) {
+    const Tile& t = k2[k];
+    if (!B.mat_ok("scale_convert", t)) return B.st;
+    const MatPlan& q = L.mats[t.mat];
+    const bool tall_list = int64_t(k) >= L.n_k2w;
+    if (!B.cond(q.tall == tall_list && t.ti >= 0 && t.ti < q.k2_tr && t.tj >= 0 && t.tj < q.k2_tc, "scale_convert",
+                t, "tile outside the grid or in the other kernel's list"))
+      return B.st;
+    const uint64_t xsz = u2 * q.mp * q.np;
+    if (!tall_list) {
+      const uint64_t r0 = uint64_t(t.ti) * K2W_R, c0 = uint64_t(t.tj) * EW_TC;
+      if (!B.erange("scale_convert_wide", "X0", t, u2 * (r0 * q.np + c0), u2 * ((r0 + K2W_R - 1) * q.np + c0 + EW_TC),
+                   xsz) ||
+          !B.erange("scale_convert_wide", "norm partials", t, 8 * uint64_t(t.idx), 8 * uint64_t(t.idx) + 8,
+                   8 * uint64_t(q.k2_tiles)))
+        return B.st;
+    } else if ((k - L.n_k2w) % K2_GROUP == 0) {
+      // A workgroup takes K2_GROUP consecutive entries: one band of one matrix.
+      for (int j = 1; j < K2_GROUP; ++j) {
+        const bool in = k + j < k2.size();
+        if (!B.cond(in && k2[k + j].mat == t.mat && k2[k + j].ti == t.ti && k2[k + j].tj == t.tj + j &&
+                        k2[k + j].idx == t.idx + j,
+                    "scale_convert_tall", t, "group entries are not consecutive tiles of one band"))
+          return B.st;
+      }
+      const uint64_t r0 = uint64_t(t.ti) * K2_T, cb = uint64_t(t.tj) * K2_T;   // W rows, W columns
+      if (!B.erange("scale_convert_tall", "X0", t, u2 * (cb * q.np + r0),
+                   u2 * ((cb + K2_GROUP * K2_T - 1) * q.np + r0 + K2_T), xsz) ||
+          !B.erange("scale_convert_tall", "norm partials", t, 8 * uint64_t(t.idx),
+                   8 * (uint64_t(t.idx) + K2_GROUP), 8 * uint64_t(q.k2_tiles)))
+        return B.st;
+    }
+  }
+  if (!B.cond((L.n_k2 - L.n_k2w) % K2_GROUP == 0, "scale_convert_tall", Tile{-1, 0, 0, 0},
+              "tall tile count is not a multiple of the group"))
+    return B.st;
+
+  // Newton-Schulz Gram and polynomial: direct loads of both panels over the
+  // whole contraction, the polynomial's reload of A's tile, and the stores of
+  // the tile and its mirror.
+  for (int phase = 0; phase < 2; ++phase) {
+    const std::vector<Tile>& list = phase == 0 ? gram : poly;
+    const char* kname = phase == 0 ? "ns_gram" : "ns_poly";
+    if (!B.cond(list.size() % NXCD == 0, kname, Tile{-1, 0, 0, 0}, "dispatch list not a multiple of the XCDs"))
+      return B.st;
+    for (const Tile& t : list) {
+      if (t.mat < 0) continue;   // padding: the workgroup returns at once
+      if (!B.mat_ok(kname, t)) return B.st;
+      const MatPlan& q = L.mats[t.mat];
+      const int T = int(q.mp / NS_TILE);
+      if (!B.cond(!q.small && t.ti >= 0 && t.ti <= t.tj && t.tj < T, kname, t, "not an upper tile of the matrix"))
+        return B.st;
+      const int row0 = t.ti * NS_TILE, col0 = t.tj * NS_TILE;
+      const int ld = phase == 0 ? int(q.np) : int(q.mp);
+      const uint64_t psz = u2 * q.mp * ld;   // X[src] (Gram) or A (polynomial)
+      const int KT = ld / ns::SymGeom::BK;
+      const bool diag = t.ti == t.tj;
+      const int nloads = (diag ? ns::SymGeom::LOADS / 2 : ns::SymGeom::LOADS) * NW;   // g = wave + NW q
+      uint64_t vmax = 0;
+      for (int g = 0; g < nloads; ++g)
+        for (int lane = 0; lane < LANES; ++lane) vmax = std::max(vmax, SL::voff(g, lane, row0, col0, ld));
+      if (!B.range(kname, phase == 0 ? "X panels" : "A panels", t, 0, vmax + SL::soff(KT - 1) + 16, psz, true))
+        return B.st;
+      if (phase == 1) {
+        uint64_t amax = 0;
+        for (int c = 0; c < NS_TILE * NS_TILE * 2 / 16; ++c)
+          amax = std::max(amax, ns::poly_a_tile_off(c, row0, col0, int(q.mp)));
+        if (!B.range(kname, "A tile", t, 0, amax + 16, u2 * q.mp * q.mp, true)) return B.st;
+      }
+      const uint64_t ldo = (phase == 1 && q.split) ? 2 * q.mp : q.mp;
+      const uint64_t off = (phase == 1 && q.split) ? q.mp : 0;   // the low part of a split B'
+      const uint64_t far = uint64_t(std::max(row0, col0)) + NS_TILE;
+      if (!B.range(kname, phase == 0 ? "A (tile and mirror)" : "B' (tile and mirror)", t,
+                   u2 * (uint64_t(std::min(row0, col0)) * ldo), u2 * ((far - 1) * ldo + off + far), u2 * q.mp * ldo))
+        return B.st;
+    }
+  }
+  // Newton-Schulz update: B' rows and X k-rows over the contraction (X's k
+  // wraps at mp for split matrices), the X' tile, the graft partial slot.
+  if (!B.cond(updd.size() % NXCD == 0, "ns_update", Tile{-1, 0, 0, 0}, "dispatch list not a multiple of the XCDs"))
+    return B.st;
+  for (const Tile& t : updd) {
+    if (t.mat < 0) continue;
+    if (!B.mat_ok("ns_update", t)) return B.st;
+    const MatPlan& q = L.mats[t.mat];
+    if (!B.cond(!q.small && t.ti >= 0 && t.ti < q.mp / NS_TILE && t.tj >= 0 && t.tj < q.np / NS_TILE &&
+                    t.idx >= 0 && t.idx < q.upd_tiles,
+                "ns_update", t, "tile outside the matrix or partial slot out of range"))
+      return B.st;
+    const int row0 = t.ti * NS_TILE, col0 = t.tj * NS_TILE;
+    const int ldb = int(q.split ? 2 * q.mp : q.mp);
+    const int KT = ldb / ns::UpdGeom::BK;
+    uint64_t bmax = 0, xmax = 0, sxmax = 0;
+    for (int g = 0; g < ns::UpdGeom::LOADS * NW; ++g)
+      for (int lane = 0; lane < LANES; ++lane) {
+        if (g < UL::LOADS_P) bmax = std::max(bmax, UL::voff_b(g, lane, row0, ldb));
+        else xmax = std::max(xmax, UL::voff_x(g, lane, col0, int(q.np)));
+      }
+    for (int kt = 0; kt < KT; ++kt) sxmax = std::max(sxmax, UL::soff_x(kt, int(q.mp), int(q.np)));
+    if (!B.range("ns_update", "B' rows", t, 0, bmax + UL::soff_b(KT - 1) + 16, u2 * q.mp * ldb, true) ||
+        !B.range("ns_update", "X k-rows", t, 0, xmax + sxmax + 16, u2 * q.mp * q.np, true) ||
+        !B.range("ns_update", "X' tile", t, u2 * (uint64_t(row0) * q.np + col0),
+                 u2 * (uint64_t(row0 + NS_TILE - 1) * q.np + col0 + NS_TILE), u2 * q.mp * q.np) ||
+        !B.range("ns_update", "graft partials", t, 8 * uint64_t(t.idx), 8 * uint64_t(t.idx) + 8,
+                 8 * uint64_t(q.upd_tiles)))
+      return B.st;
+  }
+  // fp32 Newton-Schulz of short sides <= 32: chunk and partial-slot indices.
+  for (const Tile& t : smg) {
+    if (!B.mat_ok("sm_gram", t)) return B.st;
+    const MatPlan& q = L.mats[t.mat];
+    if (!B.cond(q.small && t.ti >= 0 && t.ti < q.sm_gchunks && int64_t(t.ti) * SM_CH_G < q.np, "sm_gram", t,
+                "chunk out of range"))
+      return B.st;
+  }
+  for (const Tile& t : smp) {
+    if (!B.mat_ok("sm_poly", t)) return B.st;
+    if (!B.cond(L.mats[t.mat].small, "sm_poly", t, "matrix is not on the fp32 path")) return B.st;
+  }
+  for (const Tile& t : smu) {
+    if (!B.mat_ok("sm_update", t)) return B.st;
+    const MatPlan& q = L.mats[t.mat];
+    if (!B.cond(q.small && t.ti >= 0 && int64_t(t.ti + 1) * SM_CH_U <= q.np && t.idx >= 0 && t.idx < q.upd_tiles,
+                "sm_update", t, "chunk or partial slot out of range"))
+      return B.st;
+  }
+  *checked = B.checked;
+  return MALT_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -776,6 +1022,19 @@ hip_error:
   return hip_fail(e, "launching step kernels");
 }
 
+malt_status_t malt_check_bounds(const malt_shape_t* shapes, int32_t n, malt_variant_t variant, int64_t shrink_bytes,
+                                int64_t* ranges_checked) {
+  if (variant != MALT_VARIANT_MALT && variant != MALT_VARIANT_MALTER)
+    return fail(MALT_ERR_INVALID_ARG, "unknown variant %d", int(variant));
+  if (!ranges_checked) return fail(MALT_ERR_INVALID_ARG, "ranges_checked is NULL");
+  if (shrink_bytes < 0) return fail(MALT_ERR_INVALID_ARG, "shrink_bytes must be >= 0");
+  *ranges_checked = 0;
+  malt_status_t st = check_shapes(shapes, n);
+  if (st != MALT_OK) return st;
+  const Layout L = make_layout(shapes, n, variant);
+  return check_bounds(L, shrink_bytes, ranges_checked);
+}
+
 malt_status_t malt_state_layout(const malt_plan_t* p, int32_t i, malt_state_layout_t* out) {
   if (!p || !out) return fail(MALT_ERR_INVALID_ARG, "NULL argument");
   if (i < 0 || i >= p->n) return fail(MALT_ERR_INVALID_ARG, "matrix index %d out of range", i);
@@ -857,6 +1116,7 @@ const char* malt_status_string(malt_status_t s) {
     case MALT_ERR_HIP: return "MALT_ERR_HIP";
     case MALT_ERR_ALIAS: return "MALT_ERR_ALIAS";
     case MALT_ERR_SCRATCH_SIZE: return "MALT_ERR_SCRATCH_SIZE";
+    case MALT_ERR_BOUNDS: return "MALT_ERR_BOUNDS";
   }
   return "MALT_ERR_UNKNOWN";
 }

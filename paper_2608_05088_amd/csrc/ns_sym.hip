@@ -1,0 +1,381 @@
+// Gram and polynomial phases of Newton-Schulz (Muon's quintic, the Orth step
+// of Sec. 3.1) on the canonical X (mp x np, rows <= cols, zero-padded to
+// multiples of 256), each one grouped launch over every matrix of the step:
+//   Gram        A  = s X X^T                 NT product, symmetric: upper tiles
+//                                            only, mirrored on write; s = sigma^2
+//                                            on the first iteration, else 1
+//   Polynomial  B' = a I + b A + c A A^T     NT product (A is symmetric, so
+//                                            A A = A A^T); upper tiles, mirrored
+// The update X' = s B' X (ns_update.hip) then needs no addend: a X is folded
+// into B', so every iteration applies one rounded matrix to one rounded X.
+// A and B' are bf16 (round to nearest even).  Stages of 64 k in a two-slot
+// ring: the Gram contracts over K = n', up to 80 stages, and gains from the
+// fewer barriers of the longer stage.
+#include "ns_common.h"
+
+namespace malt {
+
+using namespace ns;
+
+namespace {
+
+using G = SymGeom;
+using L = SymLoads<G>;
+constexpr int BK = G::BK, STAGES = G::STAGES, H = G::H, RB = G::RB, CPR = G::CPR, RPP = G::RPP;
+constexpr int OPER_BYTES = G::OPER_BYTES, STAGE_BYTES = G::STAGE_BYTES, LOADS = G::LOADS;
+__device__ __forceinline__ int swz_rk(int row, int kc) { return G::swz_rk(row, kc); }
+
+// Epilogue staging.  A diagonal tile stages the whole bf16 tile in LDS and
+// writes it out in 512-byte rows: written column-wise (each lane: four
+// consecutive rows of one column, 8 bytes into one staged row), rows padded by
+// 8 bytes so the 32 staged rows of one write land in distinct banks; written
+// row-wise (each lane: four consecutive columns), rows padded by 64 bytes.
+// Off-diagonal tiles go through per-wave regions: the sub-tile transposed (TN
+// rows of TM bf16, padded by 8 bytes), then as is (TM rows of TN bf16,
+// unpadded, halves swapped on alternate row pairs).
+constexpr int ST_PITCH_T = NS_TILE * 2 + 8;
+constexpr int ST_PITCH_R = NS_TILE * 2 + 64;
+constexpr int SYM_PITCH_T = TM * 2 + 8;
+constexpr int SYM_WAVE = TN * SYM_PITCH_T > TM * TN * 2 ? TN * SYM_PITCH_T : TM * TN * 2;
+constexpr int SYM_EPI_BYTES = NS_TILE * ST_PITCH_R;
+constexpr int LDS_BYTES = G::RING_BYTES > SYM_EPI_BYTES ? G::RING_BYTES : SYM_EPI_BYTES;
+static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
+static_assert(NW * SYM_WAVE <= LDS_BYTES, "per-wave epilogue regions");
+
+}  // namespace
+
+// ===========================================================================
+// Gram and polynomial phases: C = P Q^T, symmetric output, upper tiles.
+// ===========================================================================
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
+void ns_gemm_sym_kernel(NsArgs args) {
+  constexpr int I = TM / 32, J = TN / 32;    // 32x32 blocks per wave
+
+  extern __shared__ __attribute__((aligned(16))) char lds[];
+  // Every descriptor field the tile needs is read here, before any store, so
+  // the uniform loads go through the scalar cache.
+  // The work list is in dispatch order (XCD-balanced on the host); entries
+  // with mat < 0 pad the shorter XCD runs.
+  const Tile t = args.tiles[blockIdx.x];
+  if (t.mat < 0) return;
+  const MatDesc* __restrict__ d = args.desc + t.mat;
+  const int phase = args.phase;
+  const int mp = d->mp, np = d->np;
+  const bool split = d->split != 0;
+  bf16_t* const Am = d->A;
+  bf16_t* const Bm = d->B;
+  const bf16_t* P = (phase == PH_GRAM) ? d->X[args.src] : Am;
+  const float sig = (args.first && phase == PH_GRAM) ? (float)d->scal[SC_SIGMA] : 1.f;
+  const int ld = (phase == PH_GRAM) ? np : mp;
+  const int K = ld;
+  const int row0 = t.ti * NS_TILE, col0 = t.tj * NS_TILE;
+  // A diagonal tile's row and column panels are the same rows of P: it loads
+  // the row panel only and reads both operands from it.
+  const bool diag = t.ti == t.tj;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // Sub-tile of each wave. On a diagonal tile only the 32 x 32 blocks on or
+  // above the block diagonal are computed (the others are their mirrors). The
+  // two waves that share a SIMD (waves w and w + 4) then take sub-tiles with
+  // 8 + 0, 8 + 0, 7 + 3 and 3 + 7 such blocks, instead of the 3 + 0, 7 + 0,
+  // 8 + 3 and 8 + 7 of the plain order, so every matrix core gets a share.
+  const int role = diag ? ((0x76540132u >> (4 * wave)) & 0xF) : wave;
+  const int wr = role / (NW / 2), wc = role % (NW / 2);
+
+  // Direct-load sources: load g < LOADS_PER_OPER covers rows of the tile-row
+  // panel, the rest rows of the tile-column panel (both of P); 32-bit byte
+  // offsets into P's buffer (SymLoads, shared with the host bounds check).
+  const i32x4 rsP = buf_rsrc(P);
+  uint32_t voff[LOADS];
+  int dst_off[LOADS];
+#pragma unroll
+  for (int q = 0; q < LOADS; ++q) {
+    const int g = wave + q * NW;
+    voff[q] = (uint32_t)L::voff(g, lane, row0, col0, ld);
+    dst_off[q] = L::dst(g);
+  }
+  int offa[I][H], offb[J][H];
+#pragma unroll
+  for (int h = 0; h < H; ++h) {
+    const int kc = 2 * h + (lane >> 5);
+#pragma unroll
+    for (int i = 0; i < I; ++i) offa[i][h] = swz_rk(wr * TM + i * 32 + (lane & 31), kc);
+#pragma unroll
+    for (int j = 0; j < J; ++j) offb[j][h] = (diag ? 0 : OPER_BYTES) + swz_rk(wc * TN + j * 32 + (lane & 31), kc);
+  }
+
+  f32x16 acc[I][J];
+#pragma unroll
+  for (int i = 0; i < I; ++i)
+#pragma unroll
+    for (int j = 0; j < J; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+  bf16x8 fa[2][I], fb[2][J];
+
+  // With 8 waves, g = wave + 8q < LOADS_PER_OPER exactly for q < LOADS / 2:
+  // the first half of a wave's loads are row-panel loads (SymLoads asserts it).
+  // Diagonal and off-diagonal tiles run separate copies of the main loop, so
+  // the block test exists only on diagonal tiles.
+  auto main_loop = [&](auto diag_tag) {
+    constexpr bool DIAG = decltype(diag_tag)::value;
+    pipeline<G, 1>(
+        K / BK, DIAG ? LOADS / 2 : LOADS, lds,
+        [&](int kt, int i) {   // diagonal tiles issue the row-panel loads q < LOADS / 2 only
+          dma16(rsP, voff[i], (uint32_t)L::soff(kt), lds_u32(lds + (kt % STAGES) * STAGE_BYTES + dst_off[i]));
+        },
+        [&](int buf, const char* st, int h) {
+#pragma unroll
+          for (int i = 0; i < I; ++i) fa[buf][i] = *reinterpret_cast<const bf16x8*>(st + offa[i][h]);
+#pragma unroll
+          for (int j = 0; j < J; ++j) fb[buf][j] = *reinterpret_cast<const bf16x8*>(st + offb[j][h]);
+        },
+        [&](int buf, auto&& after) {
+#pragma unroll
+          for (int i = 0; i < I; ++i)
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+              // Diagonal tiles skip the blocks below the block diagonal.
+              if (!DIAG || (wr * TM) / 32 + i <= (wc * TN) / 32 + j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[buf][i], fb[buf][j], acc[i][j], 0, 0, 0);
+              after(i * J + j);
+            }
+        });
+  };
+  if (diag) main_loop(std::true_type{});
+  else main_loop(std::false_type{});
+
+  // ---------------------------------------------------------------- epilogue
+  // acc[i][j][4g + e] = C(r, c): tile row r = wr*TM + i*32 + 8g + 4*(lane >> 5)
+  // + e, tile column c = wc*TN + j*32 + (lane & 31), so each lane holds four
+  // consecutive rows of one column.  The final bf16 values are formed in
+  // registers; the tile then leaves through LDS twice in whole rows: first
+  // transposed (the mirror tile C^T), then as is after a 4 x 4 transpose
+  // inside each lane quad. A diagonal tile is its own mirror and leaves once:
+  // its staged copy takes the computed blocks transposed and the blocks above
+  // the block diagonal as is, so it is symmetric by construction.
+  const bool poly = phase == PH_POLY;
+  const float sc = sig * sig;
+  // Split B': the low part bf16(v - hi) goes mp columns to the right.
+  const int lo_off = (poly && split) ? mp : 0;
+  bf16_t* const out = poly ? Bm : Am;
+  const int ldo = lo_off ? 2 * mp : mp;
+  const int rl0 = wr * TM + 4 * (lane >> 5);   // tile row of i = g = e = 0
+  const int cl0 = wc * TN + (lane & 31);       // tile column of j = 0
+
+  __syncthreads();   // every wave is done reading the operand ring
+  if (poly) {
+    // B' = a I + b A + c A A^T takes A(r, c) at each accumulator position.
+    // A's tile goes to LDS as 256 rows in the [k][n] layout (direct loads),
+    // and each lane reads its four rows of one column with one transposed
+    // read per (i, j, g).
+    const i32x4 rsA = buf_rsrc(Am);
+#pragma unroll
+    for (int it = 0; it < NS_TILE * NS_TILE * 2 / (16 * NT); ++it) {
+      const int c = tid + NT * it;   // 16-byte chunk of the tile; physical chunk c & 31 of
+                                     // row c >> 5 holds logical chunk (c & 31) ^ 4 (row & 3)
+      dma16(rsA, (uint32_t)poly_a_tile_off(c, row0, col0, mp), 0u, lds_u32(lds + (c - lane) * 16));
+    }
+    wait_vm_c<0>();
+    __syncthreads();
+  }
+  uint2 hv[I][J][4];
+  {
+    const int r = (lane & 15) >> 2, q = lane & 3;
+#pragma unroll
+    for (int i = 0; i < I; ++i)
+#pragma unroll
+      for (int j = 0; j < J; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * g + e];
+          if (poly) {
+            const int k0 = rl0 + i * 32 + 8 * g;
+            const int n0 = wc * TN + j * 32 + 16 * ((lane >> 4) & 1);
+            const i16x4 av = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(lds + swz_kn(k0 + r, n0 + 4 * q)));
+            const int R = row0 + k0, C = col0 + cl0 + j * 32;
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              v[e] = args.b * bf2f_((bf16_t)av[e]) + args.c * v[e] + (R + e == C ? args.a : 0.f);
+          }
+          hv[i][j][g].x = pack_bf16x2(sc * v[0], sc * v[1]);
+          hv[i][j][g].y = pack_bf16x2(sc * v[2], sc * v[3]);
+          if (lo_off) {
+            // Keep the low parts in acc (its values are no longer needed).
+            acc[i][j][4 * g + 0] = sc * v[0] - bf16_lo(hv[i][j][g].x);
+            acc[i][j][4 * g + 1] = sc * v[1] - bf16_hi(hv[i][j][g].x);
+            acc[i][j][4 * g + 2] = sc * v[2] - bf16_lo(hv[i][j][g].y);
+            acc[i][j][4 * g + 3] = sc * v[3] - bf16_hi(hv[i][j][g].y);
+          }
+        }
+  }
+
+  // Row-wise copy of accumulator group (i, j, g): a 4 x 4 transpose of
+  // 16-bit values inside each lane quad, after which lane p of the quad holds
+  // row p of the quad's four rows, its four columns.
+  const int p = lane & 3;
+  auto quad_rows = [&](int i, int j, int g) {
+    const uint32_t A0 = hv[i][j][g].x, B0 = hv[i][j][g].y;   // rows (0,1), (2,3) of column p
+    const uint32_t A1 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)A0, 0xB1, 0xF, 0xF, true);   // lane p ^ 1
+    const uint32_t B1 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)B0, 0xB1, 0xF, 0xF, true);
+    // Even lanes: row 0 (A) / row 2 (B) at columns p, p+1; odd lanes:
+    // row 1 / row 3 at columns p-1, p.
+    const uint32_t nA = (p & 1) ? ((A1 >> 16) | (A0 & 0xffff0000u)) : ((A0 & 0xffffu) | (A1 << 16));
+    const uint32_t nB = (p & 1) ? ((B1 >> 16) | (B0 & 0xffff0000u)) : ((B0 & 0xffffu) | (B1 << 16));
+    const uint32_t S = (p < 2) ? nB : nA;
+    const uint32_t S2 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)S, 0x4E, 0xF, 0xF, true);   // lane p ^ 2
+    return (p < 2) ? make_uint2(nA, S2) : make_uint2(S2, nB);
+  };
+  // Writes one set of values (hi, or the split low part at column offset
+  // off): the transposed staging first, then the row-wise one.
+  auto emit = [&](int off) {
+    constexpr int CHUNKS = NS_TILE * NS_TILE * 2 / 16;
+    __syncthreads();   // LDS free (A's tile read, or the previous copy-out done)
+    if constexpr (TM == 128 && TN == 64) {   // the layout below assumes 128 x 64 wave blocks
+      if (!diag) {
+        // Off-diagonal tile: each wave moves its own TM x TN block through a
+        // private LDS region, first transposed (to the mirror tile), then as
+        // is.  A wave reads back only what it wrote and LDS operations of one
+        // wave stay in order, so no barrier separates the phases.  Outputs are
+        // written with streaming stores, as in the update: the next phase
+        // reads them from other XCDs.
+        char* const wreg = lds + wave * SYM_WAVE;
+#pragma unroll
+        for (int i = 0; i < I; ++i)
+#pragma unroll
+          for (int j = 0; j < J; ++j)
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+              *reinterpret_cast<uint2*>(wreg + ((lane & 31) + j * 32) * SYM_PITCH_T +
+                                        (4 * (lane >> 5) + i * 32 + 8 * g) * 2) = hv[i][j][g];
+        // Mirror: staged row x (of TM bf16) goes to row col0 + wc*TN + x.
+        constexpr int TCH = TM * 2 / 16;
+#pragma unroll
+        for (int it = 0; it < TN * TCH / 64; ++it) {
+          const int q = lane + 64 * it;
+          const int r = q / TCH, ch = q % TCH;
+          const char* src = wreg + r * SYM_PITCH_T + ch * 16;
+          const uint2 lo = *reinterpret_cast<const uint2*>(src);
+          const uint2 hi = *reinterpret_cast<const uint2*>(src + 8);
+          const u32x4 v = {lo.x, lo.y, hi.x, hi.y};
+          __builtin_nontemporal_store(v, reinterpret_cast<MALT_GLOBAL u32x4*>(
+                                             gptr(out) + (size_t)(col0 + wc * TN + r) * ldo + off + row0 + wr * TM + ch * 8));
+        }
+        // As is: 128-byte rows; rows 2 and 3 (mod 4) hold their two 64-byte
+        // halves swapped, so the four rows of one quad write land in four
+        // distinct 16-bank groups.
+#pragma unroll
+        for (int i = 0; i < I; ++i)
+#pragma unroll
+          for (int j = 0; j < J; ++j)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+              const int r = 4 * (lane >> 5) + i * 32 + 8 * g + p;
+              const int hf = j ^ ((r >> 1) & 1);
+              *reinterpret_cast<uint2*>(wreg + r * (TN * 2) + hf * 64 + (((lane & 31) >> 2) << 3)) =
+                  quad_rows(i, j, g);
+            }
+        constexpr int DCH = TN * 2 / 16;
+#pragma unroll
+        for (int it = 0; it < TM * DCH / 64; ++it) {
+          const int q = lane + 64 * it;
+          const int r = q / DCH, ch = q % DCH;
+          const int hf = (ch >> 2) ^ ((r >> 1) & 1);
+          const u32x4 v = *reinterpret_cast<const u32x4*>(wreg + r * (TN * 2) + hf * 64 + (ch & 3) * 16);
+          __builtin_nontemporal_store(v, reinterpret_cast<MALT_GLOBAL u32x4*>(
+                                             gptr(out) + (size_t)(row0 + wr * TM + r) * ldo + off + col0 + wc * TN + ch * 8));
+        }
+        return;
+      }
+    }
+    // Transposed staging: staged row x is tile column x. A diagonal tile
+    // stages only its computed blocks this way (block row <= block column) and
+    // stages the blocks above the block diagonal also as is, at the places of
+    // their skipped mirrors: the staged tile is then the whole symmetric tile.
+#pragma unroll
+    for (int i = 0; i < I; ++i)
+#pragma unroll
+      for (int j = 0; j < J; ++j) {
+        const int br = (wr * TM) / 32 + i, bc = (wc * TN) / 32 + j;   // wave-uniform block coordinates
+        if (!diag || br <= bc)
+#pragma unroll
+          for (int g = 0; g < 4; ++g)
+            *reinterpret_cast<uint2*>(lds + (cl0 + j * 32) * ST_PITCH_T + (rl0 + i * 32 + 8 * g) * 2) = hv[i][j][g];
+        if (diag && br < bc)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const int rr = rl0 + i * 32 + 8 * g + p;
+            const int cc = wc * TN + j * 32 + ((lane & 31) & ~3);
+            *reinterpret_cast<uint2*>(lds + rr * ST_PITCH_T + cc * 2) = quad_rows(i, j, g);
+          }
+      }
+    __syncthreads();
+    // Staged row x goes to row col0 + x (the mirror tile; on a diagonal tile,
+    // the tile itself).
+#pragma unroll 4
+    for (int c = tid; c < CHUNKS; c += NT) {
+      const int row = c >> 5, ch = c & 31;
+      const char* src = lds + row * ST_PITCH_T + ch * 16;
+      const uint2 lo = *reinterpret_cast<const uint2*>(src);
+      const uint2 hi = *reinterpret_cast<const uint2*>(src + 8);
+      const u32x4 v = {lo.x, lo.y, hi.x, hi.y};
+      __builtin_nontemporal_store(
+          v, reinterpret_cast<MALT_GLOBAL u32x4*>(gptr(out) + (size_t)(col0 + row) * ldo + off + row0 + ch * 8));
+    }
+    if (diag) return;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < I; ++i)
+#pragma unroll
+      for (int j = 0; j < J; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int rr = rl0 + i * 32 + 8 * g + p;
+          const int cc = wc * TN + j * 32 + ((lane & 31) & ~3);
+          *reinterpret_cast<uint2*>(lds + rr * ST_PITCH_R + cc * 2) = quad_rows(i, j, g);
+        }
+    __syncthreads();
+#pragma unroll 4
+    for (int c = tid; c < CHUNKS; c += NT) {
+      const int row = c >> 5, ch = c & 31;
+      __builtin_nontemporal_store(*reinterpret_cast<const u32x4*>(lds + row * ST_PITCH_R + ch * 16),
+                                  reinterpret_cast<MALT_GLOBAL u32x4*>(gptr(out) + (size_t)(row0 + row) * ldo + off +
+                                                                       col0 + ch * 8));
+    }
+  };
+  emit(0);
+  if (lo_off) {
+#pragma unroll
+    for (int i = 0; i < I; ++i)
+#pragma unroll
+      for (int j = 0; j < J; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          hv[i][j][g].x = pack_bf16x2(acc[i][j][4 * g + 0], acc[i][j][4 * g + 1]);
+          hv[i][j][g].y = pack_bf16x2(acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+        }
+    emit(lo_off);
+  }
+}
+
+
+// The kernel uses more dynamic LDS than the default limit; the attribute is
+// set for the current device (plan set-up calls ns_gemm_setup with the plan's
+// device current, so every device a plan runs on has it).
+hipError_t ns_gemm_setup() {
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&ns_gemm_sym_kernel),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
+  if (e == hipSuccess) e = ns_update_setup();
+  return e;
+}
+
+hipError_t launch_ns_gemm(const NsArgs& a, hipStream_t s) {
+  if (a.ntiles == 0) return hipSuccess;
+  if (a.phase == PH_UPDATE) return launch_ns_update(a, s);
+  hipLaunchKernelGGL(ns_gemm_sym_kernel, dim3(a.ntiles), dim3(NT), LDS_BYTES, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace malt

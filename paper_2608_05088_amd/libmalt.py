@@ -23,6 +23,7 @@ MALT_ERR_STATE_MISMATCH = 4
 MALT_ERR_HIP = 5
 MALT_ERR_ALIAS = 6
 MALT_ERR_SCRATCH_SIZE = 7
+MALT_ERR_BOUNDS = 8
 MALT_SCRATCH_BYTES = 64 << 20
 
 MALT_VARIANT_MALT = 0
@@ -85,6 +86,7 @@ _SIGNATURES = [
     ("malt_state_layout", c_int32, [c_void_p, c_int32, POINTER(malt_state_layout_t)]),
     ("malt_debug_layout", c_int32, [c_void_p, c_int32, POINTER(malt_debug_layout_t)]),
     ("malt_plan_step", c_int64, [c_void_p]),
+    ("malt_check_bounds", c_int32, [POINTER(malt_shape_t), c_int32, c_int32, c_int64, POINTER(c_int64)]),
     ("malt_profile_enable", c_int32, [c_void_p, c_int32]),
     ("malt_profile_read", c_int32, [c_void_p, POINTER(malt_profile_t), c_int32]),
     ("malt_destroy_state", None, [c_void_p]),
@@ -152,6 +154,16 @@ def malt_state_size(shapes: Sequence[Tuple[int, int]], variant: str = "malt") ->
     _check(lib().malt_state_size(_shapes(shapes), len(shapes), VARIANTS[variant], ctypes.byref(sb),
                                  ctypes.byref(wb)))
     return sb.value, wb.value
+
+
+def check_bounds(shapes: Sequence[Tuple[int, int]], variant: str = "malt", shrink_bytes: int = 0) -> int:
+    """malt_check_bounds: the number of address ranges proved in bounds for a
+    plan over `shapes`; raises MaltError (MALT_ERR_BOUNDS) naming the first
+    range that is not.  Host only."""
+    checked = c_int64(0)
+    _check(lib().malt_check_bounds(_shapes(shapes), len(shapes), VARIANTS[variant], int(shrink_bytes),
+                                   ctypes.byref(checked)))
+    return checked.value
 
 
 def _stream_handle(stream) -> Optional[int]:
