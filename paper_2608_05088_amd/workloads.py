@@ -28,6 +28,7 @@ import numpy as np
 
 WEIGHT_KEY = 2_000_000_001     # SeedSequence key for initial weights
 ROWSCALE_KEY = 2_000_000_002   # SeedSequence key for per-row gradient scales
+LOWRANK_KEY = 2_000_000_003    # SeedSequence key for the low-rank factors
 GRAD_SCALE = 1e-2
 WEIGHT_STD = 0.02
 
@@ -93,11 +94,30 @@ def grad(cid: int, step: int, idx: int, shape: Shape, dist: str = "normal",
     elif dist == "student_t3":
         x = g.standard_t(3.0, size=(m, n))
         x *= scale
+    elif dist.startswith("lowrank"):
+        x = lowrank(cid, idx, shape, dist, g)
+        x *= scale
     elif dist == "zero":
         x = np.zeros((m, n))
     else:
         raise ValueError(f"unknown distribution {dist!r}")
     return x.astype(np.float32)
+
+
+def lowrank(cid: int, idx: int, shape: Shape, dist: str, g: np.random.Generator) -> np.ndarray:
+    """"lowrank<r>_<noise>": a rank-r matrix U V^T (factors N(0,1), drawn once per
+    matrix, so successive steps share the dominant subspace, as the gradients
+    of a real layer do) plus `noise` times an N(0, r) matrix drawn per step:
+    the noise floor sits `noise` below the low-rank part, entry for entry."""
+    m, n = shape
+    r_s, noise_s = dist[len("lowrank"):].split("_")
+    r, noise = int(r_s), float(noise_s)
+    f = _rng(cid, LOWRANK_KEY, idx)
+    u = f.standard_normal((m, r))
+    v = f.standard_normal((r, n))
+    x = u @ v
+    x += (noise * np.sqrt(r)) * g.standard_normal((m, n))
+    return x
 
 
 def weight(cid: int, idx: int, shape: Shape, std: float = WEIGHT_STD) -> np.ndarray:
