@@ -229,10 +229,13 @@ __global__ __launch_bounds__(K2W_THREADS) void scale_convert_wide_kernel(EwArgs 
 // Each thread converts two consecutive W rows of four W columns per tile, so
 // it holds, per W column, the two bf16 values of one 32-bit word of the
 // canonical row (canonical columns 2p, 2p + 1).  The words go to LDS as
-// [canonical row][word] with a pitch of 33 words: the 64 lanes of a write
-// (16 column groups x 4 row pairs) hit 64 distinct banks.  The copy-out reads
-// 16-byte row pieces back as four words (at most 2-way bank conflicts) and
-// stores 128-byte row pieces of X0.
+// [canonical row][word], word p of row c rotated to (p + 2 (c / 4) + c % 4)
+// mod 32 (tall_word): the 32 lanes of each half-wave hit 32 distinct banks,
+// both when writing (16 column groups x 2 row pairs) and when the copy-out
+// reads its 16-byte row pieces back as four words.  X0 leaves in 128-byte row
+// pieces.
+__device__ __forceinline__ int tall_word(int c, int p) { return c * (K2_T / 2) + ((p + 2 * (c >> 2) + (c & 3)) & (K2_T / 2 - 1)); }
+
 template <bool MALTER>
 __global__ __launch_bounds__(K2T_THREADS) void scale_convert_tall_kernel(EwArgs a) {
   constexpr int TG = K2_GROUP;
@@ -240,11 +243,11 @@ __global__ __launch_bounds__(K2T_THREADS) void scale_convert_tall_kernel(EwArgs 
   constexpr int NP = K2T_THREADS / 16;         // row pairs per pass: 16 threads x 4 columns span 64 columns
   constexpr int PASSES = K2_T / (2 * NP);      // row-pair passes per tile
   constexpr int WPR = K2_T / 2;                // words per canonical row of a tile
-  constexpr int PITCH = WPR + 1;               // LDS words per staged canonical row
   constexpr int CPR = WPR / 4;                 // 16-byte pieces per canonical row of a tile
   constexpr int ROWS_OUT = K2T_THREADS / CPR;  // canonical rows per copy-out pass
   static_assert(PASSES * 2 * NP == K2_T && K2_T % ROWS_OUT == 0, "tall tile layout");
-  __shared__ uint32_t tsh[TG][K2_T][PITCH];
+  static_assert(WPR == 32, "tall_word rotates within 32-word rows");
+  __shared__ uint32_t tsh[TG][K2_T * WPR];
   __shared__ float red[2 * TG][NW];
   const int grp = xcd_remap(blockIdx.x, gridDim.x);
   const Tile t = a.tiles[grp * TG];
@@ -313,7 +316,7 @@ __global__ __launch_bounds__(K2T_THREADS) void scale_convert_tall_kernel(EwArgs 
           }
         }
 #pragma unroll
-      for (int e = 0; e < 4; ++e) tsh[j][4 * cg + e][p] = pack_bf16x2(x[0][e], x[1][e]);
+      for (int e = 0; e < 4; ++e) tsh[j][tall_word(4 * cg + e, p)] = pack_bf16x2(x[0][e], x[1][e]);
     }
   }
   __syncthreads();
@@ -323,8 +326,8 @@ __global__ __launch_bounds__(K2T_THREADS) void scale_convert_tall_kernel(EwArgs 
   for (int j = 0; j < TG; ++j)
 #pragma unroll
     for (int rr = threadIdx.x / CPR; rr < K2_T; rr += ROWS_OUT) {
-      const uint32_t* src = &tsh[j][rr][4 * piece];
-      const ew_u32x4 v = {src[0], src[1], src[2], src[3]};
+      const ew_u32x4 v = {tsh[j][tall_word(rr, 4 * piece + 0)], tsh[j][tall_word(rr, 4 * piece + 1)],
+                          tsh[j][tall_word(rr, 4 * piece + 2)], tsh[j][tall_word(rr, 4 * piece + 3)]};
       __builtin_nontemporal_store(
           v, reinterpret_cast<MALT_GLOBAL ew_u32x4*>(X0 + (size_t)(cb + j * K2_T + rr) * ldx + r0 + 8 * piece));
     }
@@ -419,12 +422,13 @@ __global__ __launch_bounds__(NTHREADS) void graft_scalars_kernel(EwArgs a) {
 // canonical columns = W rows) is staged in LDS as 32-bit words, word w holding
 // W rows 2w and 2w + 1 of one W column.  bm_word() places word (c, w), with
 // c = 4 l + e, in a 64-word segment per (w, e) that holds the 64 values of l
-// rotated by 16 e + 4 (w / 4).  The fill (each thread: 16 bytes of one
+// rotated by 8 e + 2 (w / 4).  Both the fill (each thread: 16 bytes of one
 // canonical row, four words) and the read (a wave's two W rows are one word;
-// lane l reads W columns 4 l .. 4 l + 3) both hit 64 distinct banks.
+// lane l reads W columns 4 l .. 4 l + 3) then hit 32 distinct banks in each
+// half-wave.
 __device__ __forceinline__ int bm_word(int c, int w) {
   const int l = c >> 2, e = c & 3;
-  return w * EW_TC + e * 64 + ((l + 16 * e + 4 * (w >> 2)) & 63);
+  return w * EW_TC + e * 64 + ((l + 8 * e + 2 * (w >> 2)) & 63);
 }
 
 __global__ __launch_bounds__(EW_THREADS) void backmap_write_kernel(EwArgs a) {
