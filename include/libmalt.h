@@ -214,6 +214,22 @@ malt_status_t malt_debug_layout(const malt_plan_t* plan, int32_t i, malt_debug_l
 malt_status_t malt_check_bounds(const malt_shape_t* shapes, int32_t n, malt_variant_t variant,
                                 int64_t shrink_bytes, int64_t* ranges_checked);
 
+/* Condition numbers of diag(l_t) and diag(r_t) for every matrix of the plan:
+ * the quantity the paper's analysis of the diagonal preconditioners (Sec. 5.4,
+ * the figure of preconditioner condition numbers per layer) reports for the
+ * attention and MLP matrices, here for the state the last enqueued step left.
+ * kappa(diag v) = max_i v_i / min_i v_i (v >= 0 is a running mean of squares);
+ * +inf when min_i v_i = 0 (a zero row or column, or a plan that has not
+ * stepped), NaN when an entry is NaN.
+ * out: device float64 buffer of 2 * n values, 8-byte aligned, written as
+ *   [kappa_l(0), kappa_r(0), kappa_l(1), kappa_r(1), ...]; caller-owned and
+ *   not overlapping the state or workspace.
+ * Enqueued on `stream` (one small kernel) after whatever is already there;
+ * nothing waits on the host.  Errors: MALT_ERR_INVALID_ARG (NULL plan or
+ * out), MALT_ERR_ALIGNMENT, MALT_ERR_ALIAS, MALT_ERR_STATE_MISMATCH (a
+ * scratch plan whose array was taken over), MALT_ERR_HIP. */
+malt_status_t malt_precond_condition(const malt_plan_t* plan, double* out, void* stream);
+
 /* Step counter t (number of steps enqueued so far). */
 int64_t malt_plan_step(const malt_plan_t* plan);
 

@@ -398,6 +398,64 @@ __global__ __launch_bounds__(NTHREADS) void norm_scalars_kernel(EwArgs a) {
   }
 }
 
+// Condition numbers of diag(l) and diag(r) (the quantity the paper's analysis
+// of the diagonal preconditioners plots per layer): the largest entry over the
+// smallest, +inf when the smallest is 0, NaN when an entry is NaN.  One
+// workgroup per matrix; max and min are exact, so the result does not depend
+// on the reduction order.
+__device__ __forceinline__ void block_max_min(const MALT_GLOBAL float* __restrict__ x, int len, float* mx_out,
+                                              float* mn_out, int* nan_out) {
+  __shared__ float sh[2][NTHREADS / 64];
+  __shared__ int shn[NTHREADS / 64];
+  float mx = 0.f, mn = INFINITY;
+  int nan = 0;
+  for (int i = threadIdx.x; i < len; i += NTHREADS) {
+    const float y = x[i];
+    nan |= y != y;
+    mx = fmaxf(mx, y);
+    mn = fminf(mn, y);
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    mx = fmaxf(mx, __shfl_xor(mx, o));
+    mn = fminf(mn, __shfl_xor(mn, o));
+    nan |= __shfl_xor(nan, o);
+  }
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (lane == 0) {
+    sh[0][w] = mx;
+    sh[1][w] = mn;
+    shn[w] = nan;
+  }
+  __syncthreads();
+  mx = sh[0][0];
+  mn = sh[1][0];
+  nan = shn[0];
+#pragma unroll
+  for (int k = 1; k < NTHREADS / 64; ++k) {
+    mx = fmaxf(mx, sh[0][k]);
+    mn = fminf(mn, sh[1][k]);
+    nan |= shn[k];
+  }
+  __syncthreads();   // sh is reused by the next call
+  *mx_out = mx;
+  *mn_out = mn;
+  *nan_out = nan;
+}
+
+__global__ __launch_bounds__(NTHREADS) void precond_cond_kernel(const MatDesc* desc, double* out) {
+  const MatDesc& d = desc[blockIdx.x];
+  float mx[2], mn[2];
+  int nan[2];
+  block_max_min(gptr(d.l), d.m, &mx[0], &mn[0], &nan[0]);
+  block_max_min(gptr(d.r), d.n, &mx[1], &mn[1], &nan[1]);
+  if (threadIdx.x < 2) {
+    const int v = threadIdx.x;
+    double k = mn[v] > 0.f ? (double)mx[v] / (double)mn[v] : INFINITY;
+    if (nan[v]) k = NAN;
+    gptr(out)[2 * (size_t)blockIdx.x + v] = k;
+  }
+}
+
 // ||O||, ||D|| = ||L O R|| from the update-tile partials; graft and coefficient.
 __global__ __launch_bounds__(NTHREADS) void graft_scalars_kernel(EwArgs a) {
   const MatDesc& d = a.desc[blockIdx.x];
@@ -574,6 +632,11 @@ hipError_t launch_norm_scalars(const EwArgs& a, int32_t nmat, hipStream_t s) {
 hipError_t launch_graft_scalars(const EwArgs& a, int32_t nmat, hipStream_t s) {
   if (nmat == 0) return hipSuccess;
   hipLaunchKernelGGL(graft_scalars_kernel, dim3(nmat), dim3(NTHREADS), 0, s, a);
+  return hipGetLastError();
+}
+hipError_t launch_precond_cond(const MatDesc* desc, int32_t nmat, double* out, hipStream_t s) {
+  if (nmat == 0) return hipSuccess;
+  hipLaunchKernelGGL(precond_cond_kernel, dim3(nmat), dim3(NTHREADS), 0, s, desc, out);
   return hipGetLastError();
 }
 hipError_t launch_backmap_write(const EwArgs& a, hipStream_t s) {

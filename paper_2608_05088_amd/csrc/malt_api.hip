@@ -1062,6 +1062,22 @@ malt_status_t malt_debug_layout(const malt_plan_t* p, int32_t i, malt_debug_layo
   return MALT_OK;
 }
 
+malt_status_t malt_precond_condition(const malt_plan_t* p, double* out, void* stream) {
+  if (!p || !out) return fail(MALT_ERR_INVALID_ARG, "NULL argument");
+  const uintptr_t o = reinterpret_cast<uintptr_t>(out);
+  if (o % 8) return fail(MALT_ERR_ALIGNMENT, "out is not 8-byte aligned");
+  const size_t bytes = 16 * size_t(p->n);
+  if (ranges_overlap(o, bytes, reinterpret_cast<uintptr_t>(p->state), p->L.state_bytes) ||
+      ranges_overlap(o, bytes, reinterpret_cast<uintptr_t>(p->ws), p->L.ws_bytes))
+    return fail(MALT_ERR_ALIAS, "out overlaps the state or workspace");
+  if (p->scratch && !scratch_current(p->device, p->scratch_gen))
+    return fail(MALT_ERR_STATE_MISMATCH, "the static scratch of device %d now belongs to a newer plan; "
+                "this plan's workspace is gone", p->device);
+  const hipError_t e = launch_precond_cond(reinterpret_cast<const MatDesc*>(p->ws + p->L.ws_desc), p->n, out,
+                                           static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? MALT_OK : hip_fail(e, "launching the condition-number kernel");
+}
+
 int64_t malt_plan_step(const malt_plan_t* p) { return p ? p->t : -1; }
 
 malt_status_t malt_profile_enable(malt_plan_t* p, int32_t enable) {

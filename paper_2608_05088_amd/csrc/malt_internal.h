@@ -183,6 +183,7 @@ hipError_t launch_scale_convert(const EwArgs& a, bool tall, hipStream_t s);
 hipError_t launch_norm_scalars(const EwArgs& a, int32_t nmat, hipStream_t s);
 hipError_t launch_graft_scalars(const EwArgs& a, int32_t nmat, hipStream_t s);
 hipError_t launch_backmap_write(const EwArgs& a, hipStream_t s);
+hipError_t launch_precond_cond(const MatDesc* desc, int32_t nmat, double* out, hipStream_t s);
 hipError_t ns_gemm_setup();   // once per plan, on the plan's device
 hipError_t launch_ns_gemm(const NsArgs& a, hipStream_t s);
 hipError_t ns_update_setup();   // the update kernel (ns_update.hip), called by ns_gemm_setup

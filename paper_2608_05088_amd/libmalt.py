@@ -86,6 +86,7 @@ _SIGNATURES = [
     ("malt_state_layout", c_int32, [c_void_p, c_int32, POINTER(malt_state_layout_t)]),
     ("malt_debug_layout", c_int32, [c_void_p, c_int32, POINTER(malt_debug_layout_t)]),
     ("malt_plan_step", c_int64, [c_void_p]),
+    ("malt_precond_condition", c_int32, [c_void_p, c_void_p, c_void_p]),
     ("malt_check_bounds", c_int32, [POINTER(malt_shape_t), c_int32, c_int32, c_int64, POINTER(c_int64)]),
     ("malt_profile_enable", c_int32, [c_void_p, c_int32]),
     ("malt_profile_read", c_int32, [c_void_p, POINTER(malt_profile_t), c_int32]),
@@ -301,6 +302,15 @@ class Plan:
             if L.B_split:
                 views["B_lo"] = b[:, p:]
         return views
+
+    def precond_condition(self, stream=None):
+        """malt_precond_condition: an (n, 2) float64 device tensor of
+        (kappa(diag l), kappa(diag r)) per matrix, enqueued on the stream."""
+        import torch
+        out = torch.empty((len(self.shapes), 2), dtype=torch.float64, device=self.device)
+        _check(lib().malt_precond_condition(self._h, c_void_p(out.data_ptr()),
+                                            c_void_p(_stream_handle(stream))))
+        return out
 
     # -- profiling ---------------------------------------------------------------
     def profile_enable(self, enable: bool = True) -> None:

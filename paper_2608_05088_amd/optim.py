@@ -26,7 +26,7 @@ Conventions
 """
 from __future__ import annotations
 
-from typing import Callable, Dict, List, Optional
+from typing import Callable, Dict, List, Optional, Tuple
 
 import torch
 
@@ -159,6 +159,22 @@ class MALT(torch.optim.Optimizer):
             g.update(s)
         if self._adam is not None and sd.get("adamw") is not None:
             self._adam.load_state_dict(sd["adamw"])
+
+    @torch.no_grad()
+    def precond_condition(self) -> Dict[torch.Tensor, Tuple[float, float]]:
+        """kappa(diag l) and kappa(diag r) of every matrix parameter that has
+        stepped, as the paper's analysis of the diagonal preconditioners
+        (Sec. 5.4) reports them per layer and module.  One small kernel per
+        parameter group, then one copy to the host."""
+        out: Dict[torch.Tensor, Tuple[float, float]] = {}
+        for k in range(len(self.param_groups)):
+            plan = self._plans[k]
+            if plan is None:
+                continue
+            kap = plan.precond_condition(stream=torch.cuda.current_stream()).cpu()
+            for p, (kl, kr) in zip(self._mats[k], kap.tolist()):
+                out[p] = (kl, kr)
+        return out
 
     def matrix_plan(self, group: int = 0) -> Optional[lm.Plan]:
         """The libmalt plan of a parameter group (built at its first step)."""

@@ -207,3 +207,45 @@ def test_concurrent_plans_on_two_streams_match_a_single_plan():
             assert torch.equal(Ws[k][i], Wr[i]), f"plan {k}, matrix {i} differs from the single-plan run"
     for pl in plans + [ref]:
         pl.close()
+
+
+def test_precond_condition_matches_the_state_and_the_oracle():
+    """kappa(diag l), kappa(diag r) per matrix: exactly max/min of the state's
+    l and r, within the state bar of the oracle's, +inf for a zero row or a
+    plan that has not stepped; argument errors are refused on the host."""
+    import ctypes
+    import torch
+    from gpu_harness import run_oracle
+    shapes = [(300, 900), (1024, 256), (17, 5)]
+    say(f"[runtime] preconditioner condition numbers {shapes}")
+    W0 = [wl.weight(97, i, s) for i, s in enumerate(shapes)]
+    grads = [[wl.grad(97, t, i, s, "row_loguniform") for i, s in enumerate(shapes)] for t in (1, 2, 3)]
+    for Gs in grads:
+        Gs[2][4, :] = 0.0   # l_4 of the third matrix stays 0
+    plan = lm.Plan(shapes, "malt")
+    assert np.all(np.isinf(plan.precond_condition().cpu().numpy()))   # l = r = 0 before any step
+    Wd = to_dev(W0)
+    for Gs in grads:
+        plan.step(Wd, to_dev(Gs), lm.make_hparams(lr=1e-3))
+    kap = plan.precond_condition().cpu().numpy()
+    o = run_oracle(shapes, "malt", W0, grads, dict(lr=1e-3))
+    for i in range(len(shapes)):
+        _, l, r, _ = plan.state_views(i)
+        for j, (v, vo) in enumerate(((l, o[-1]["l"][i]), (r, o[-1]["r"][i]))):
+            v = v.double().cpu().numpy()
+            assert kap[i, j] == (v.max() / v.min() if v.min() > 0 else np.inf)
+            if vo.min() == 0:
+                assert np.isinf(kap[i, j])
+            else:
+                assert abs(kap[i, j] / (vo.max() / vo.min()) - 1.0) <= 1e-5
+    assert np.isinf(kap[2, 0]) and np.isfinite(kap[2, 1])
+    # Row scales over three decades spread l (squared: six) and leave r flat.
+    assert np.all(kap[:2, 0] > 1e4) and np.all(kap[:2, 1] < 10.0)
+    say(f"[runtime] kappa {kap.tolist()}")
+    out = torch.empty(8, dtype=torch.float64, device=plan.device)
+    f = lm.lib().malt_precond_condition
+    assert f(plan._h, None, None) == lm.MALT_ERR_INVALID_ARG
+    assert f(plan._h, ctypes.c_void_p(out.data_ptr() + 4), None) == lm.MALT_ERR_ALIGNMENT
+    assert f(plan._h, ctypes.c_void_p(plan.state.data_ptr()), None) == lm.MALT_ERR_ALIAS
+    torch.cuda.synchronize()
+    plan.close()
