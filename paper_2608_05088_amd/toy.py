@@ -23,6 +23,10 @@ Optimizers:
     Orth(P grad Q) Q with P = (A^T A)^(-1/2) and Q = (B^T B)^(-1/2). It uses the
     exact polar factor, in float64 on the host. It is the comparison the paper
     plots, not part of the library.
+  * "muon_polar" is Muon as the appendix defines it: X <- X - eta Orth(grad), the
+    exact polar factor with no momentum and no grafting, in float64 on the host.
+    The libmalt "muon" run is instead the library's step with L = R = I
+    (Newton-Schulz, momentum 0.95, grafting).
 
 The gradient grad f = A^T (A X B^T - C) B is formed in float64 by torch on the
 device for the libmalt runs. The figure's data is not printed, so the
@@ -106,10 +110,10 @@ def _polar(G: np.ndarray) -> np.ndarray:
     return (u[:, keep] @ vt[keep]) if keep.any() else np.zeros_like(G)
 
 
-def run_whitened(p: Problem, steps: int, eta_max: float = 1e-3) -> dict:
-    """The paper's exact-whitening preconditioned Muon (host, float64)."""
+def _run_polar(p: Problem, steps: int, P: np.ndarray, Q: np.ndarray, eta_max: float) -> dict:
+    """X <- X - eta_t P Orth(P grad Q) Q with the exact polar factor, no momentum
+    (host, float64)."""
     sched = wsd(steps // 10, steps - steps // 10 - steps // 5, steps // 5)
-    P, Q = _inv_sqrt_psd(p.A.T @ p.A), _inv_sqrt_psd(p.B.T @ p.B)
     X = np.zeros((p.A.shape[1], p.B.shape[1]))
     fstar = p.f(p.lstsq())
     gaps = {0: p.f(X) - fstar}
@@ -118,6 +122,18 @@ def run_whitened(p: Problem, steps: int, eta_max: float = 1e-3) -> dict:
         if t in CHECKPOINTS or t == steps:
             gaps[t] = p.f(X) - fstar
     return gaps
+
+
+def run_whitened(p: Problem, steps: int, eta_max: float = 1e-3) -> dict:
+    """The paper's exact-whitening preconditioned Muon (host, float64)."""
+    return _run_polar(p, steps, _inv_sqrt_psd(p.A.T @ p.A), _inv_sqrt_psd(p.B.T @ p.B), eta_max)
+
+
+def run_polar_muon(p: Problem, steps: int, eta_max: float = 1e-3) -> dict:
+    """Muon as the appendix runs it: the exact polar factor of the gradient, no
+    momentum, no grafting (host, float64)."""
+    r = p.A.shape[1]
+    return _run_polar(p, steps, np.eye(r), np.eye(r), eta_max)
 
 
 def run_libmalt(p: Problem, steps: int, variant: str, eta_max: float = 1e-3, device=None) -> dict:
@@ -166,6 +182,7 @@ def main(argv=None):
             print(f"[toy] kappa {kappa:g} {name}", file=sys.stderr, flush=True)
             row[name] = {str(k): v for k, v in run_libmalt(p, args.steps, name).items()}
         row["whitened"] = {str(k): v for k, v in run_whitened(p, args.steps).items()}
+        row["muon_polar"] = {str(k): v for k, v in run_polar_muon(p, args.steps).items()}
         print(json.dumps(row), flush=True)
 
 

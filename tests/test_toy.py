@@ -3,7 +3,7 @@ exact-whitening comparison, pinned on the CPU; libmalt runs on the GPU."""
 import numpy as np
 import pytest
 
-from paper_2608_05088_amd.toy import make_problem, run_whitened
+from paper_2608_05088_amd.toy import make_problem, run_polar_muon, run_whitened
 
 
 @pytest.mark.parametrize("kappa", [10.0, 1e2, 1e3, 1e4])
@@ -39,6 +39,23 @@ def test_whitened_muon_does_not_see_the_condition_number():
     for t in g10:
         assert g1e4[t] == pytest.approx(g10[t], rel=1e-7, abs=1e-12)
     assert g10[400] < 0.5 * g10[0]
+
+
+def test_polar_muon_slows_as_the_condition_number_grows():
+    # The appendix's Muon (exact polar factor, no momentum) on the same
+    # problems: its gap after 1000 steps grows with kappa, while the whitened
+    # run's does not (the comparison its figure makes).
+    gaps = [run_polar_muon(make_problem(k), 1000)[1000] for k in (10.0, 1e2, 1e3, 1e4)]
+    assert all(a < b for a, b in zip(gaps, gaps[1:]))
+    w = [run_whitened(make_problem(k), 1000)[1000] for k in (10.0, 1e4)]
+    assert w[1] == pytest.approx(w[0], rel=1e-7, abs=1e-12) and w[0] < gaps[0]
+    # One step at eta_max (a 1-step schedule is all plateau): X1 = -eta Orth(G0),
+    # with Orth(G0) = G0 (G0^T G0)^(-1/2) written out from the eigenvalues.
+    p = make_problem(1e3)
+    G0 = p.grad(np.zeros((5, 5)))
+    w_, V = np.linalg.eigh(G0.T @ G0)
+    X1 = -1e-3 * G0 @ (V / np.sqrt(w_)) @ V.T
+    assert run_polar_muon(p, 1)[1] == pytest.approx(p.f(X1) - p.f(p.lstsq()), rel=1e-10)
 
 
 @pytest.mark.gpu
