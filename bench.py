@@ -11,7 +11,7 @@ HBM bandwidth / throughput, and the fp64 CPU oracle timed on a bounded sample
 of the same workload (cpu_baseline).
 
   python bench.py [--steps K] [--warmup W] [--workload gpt2_large|gpt2_small|gpt2_medium|single_256x512|stress_4096]
-                  [--no-cpu-baseline] [--no-vendor-ref] [--small-case] [--gpus 1]
+                  [--no-cpu-baseline] [--no-vendor-ref] [--no-ceiling] [--small-case] [--gpus 1]
 """
 from __future__ import annotations
 
@@ -45,6 +45,8 @@ def parse():
     ap.add_argument("--no-vendor-ref", action="store_true",
                     help="skip timing torch.bmm (hipBLASLt) on the update products")
     ap.add_argument("--cpu-sample-layers", type=int, default=12)
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the matrix-core ceiling calibration (MFMA-only kernel with random operands)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run one plain 1 GiB device-to-device copy (HBM counter calibration)")
     return ap.parse_args()
@@ -310,6 +312,17 @@ def main():
     vendor = None if args.no_vendor_ref else vendor_gemm_reference(w, dev)
     if vendor is not None:
         roofline["vendor_gemm_reference"] = vendor
+    if not args.no_ceiling:
+        # The matrix cores' sustained rate under the power budget with random
+        # bf16 operands and no memory traffic: context for the datasheet peak.
+        from paper_2608_05088_amd.calib import mfma_ceiling
+        ceil = mfma_ceiling("random")
+        roofline["power_limited_ceiling"] = {
+            "what": "MFMA-only kernel, random N(0,1) bf16 operands in registers, every CU, no memory traffic",
+            "TFLOP_per_s": ceil["TFLOP_per_s"], "clock_MHz": ceil["clock_MHz"],
+            "frac_of_peak": round(ceil["TFLOP_per_s"] / PEAK_BF16_TFLOPS, 4),
+            "update_frac_of_ceiling": round(achieved / ceil["TFLOP_per_s"], 4),
+            "newton_schulz_frac_of_ceiling": round(ns_all["TFLOP_per_s"] / ceil["TFLOP_per_s"], 4)}
     if args.copy_calibration:
         # A plain copy kernel of known size (an elementwise x*1 kernel, not the
         # SDMA engine): 2^30 bytes read, 2^30 bytes written.

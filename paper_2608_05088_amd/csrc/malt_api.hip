@@ -570,7 +570,6 @@ struct BoundsCheck {
 };
 
 malt_status_t check_bounds(const Layout& L, int64_t shrink, int64_t* checked) {
-  using SL = ns::SymLoads<ns::SymGeom>;
   using UL = ns::UpdLoads<ns::UpdGeom>;
   constexpr int NW = ns::NW, LANES = 64;
   BoundsCheck B{L, shrink};
@@ -698,14 +697,20 @@ malt_status_t check_bounds(const Layout& L, int64_t shrink, int64_t* checked) {
       const int row0 = t.ti * NS_TILE, col0 = t.tj * NS_TILE;
       const int ld = phase == 0 ? int(q.np) : int(q.mp);
       const uint64_t psz = u2 * q.mp * ld;   // X[src] (Gram) or A (polynomial)
-      const int KT = ld / ns::SymGeom::BK;
       const bool diag = t.ti == t.tj;
-      const int nloads = (diag ? ns::SymGeom::LOADS / 2 : ns::SymGeom::LOADS) * NW;   // g = wave + NW q
-      uint64_t vmax = 0;
-      for (int g = 0; g < nloads; ++g)
-        for (int lane = 0; lane < LANES; ++lane) vmax = std::max(vmax, SL::voff(g, lane, row0, col0, ld));
-      if (!B.range(kname, phase == 0 ? "X panels" : "A panels", t, 0, vmax + SL::soff(KT - 1) + 16, psz, true))
-        return B.st;
+      // The Gram's and the polynomial's pipeline geometries.
+      auto panel_span = [&](auto geom) -> uint64_t {
+        using G = decltype(geom);
+        using SL = ns::SymLoads<G>;
+        const int KT = ld / G::BK;
+        const int nloads = (diag ? G::LOADS / 2 : G::LOADS) * NW;   // g = wave + NW q
+        uint64_t vmax = 0;
+        for (int g = 0; g < nloads; ++g)
+          for (int lane = 0; lane < LANES; ++lane) vmax = std::max(vmax, SL::voff(g, lane, row0, col0, ld));
+        return vmax + SL::soff(KT - 1) + 16;
+      };
+      const uint64_t span = phase == 0 ? panel_span(ns::SymGeom{}) : panel_span(ns::PolyGeom{});
+      if (!B.range(kname, phase == 0 ? "X panels" : "A panels", t, 0, span, psz, true)) return B.st;
       if (phase == 1) {
         uint64_t amax = 0;
         for (int c = 0; c < NS_TILE * NS_TILE * 2 / 16; ++c)

@@ -75,9 +75,10 @@ __host__ __device__ constexpr int swz_kn(int k, int n) {
   return k * KN_ROW + (((n >> 3) ^ (4 * (k & 3))) << 4) + ((n & 7) << 1);
 }
 
-// The stage geometries of the two kernels.
-using SymGeom = NsGeom<64, 2>;   // Gram and polynomial (ns_sym.hip)
-using UpdGeom = NsGeom<32, 4>;   // update (ns_update.hip)
+// The stage geometries of the kernels.
+using SymGeom = NsGeom<64, 2>;    // Gram (ns_sym.hip)
+using PolyGeom = NsGeom<64, 2>;   // polynomial (ns_sym.hip; four 32-k slots measured no faster)
+using UpdGeom = NsGeom<32, 4>;    // update (ns_update.hip)
 
 // ---------------------------------------------------------------------------
 // Operand addressing of the direct loads, shared by the kernels and the

@@ -8,9 +8,10 @@
 //                                            A A = A A^T); upper tiles, mirrored
 // The update X' = s B' X (ns_update.hip) then needs no addend: a X is folded
 // into B', so every iteration applies one rounded matrix to one rounded X.
-// A and B' are bf16 (round to nearest even).  Stages of 64 k in a two-slot
-// ring: the Gram contracts over K = n', up to 80 stages, and gains from the
-// fewer barriers of the longer stage.
+// A and B' are bf16 (round to nearest even).  One kernel template, one
+// instance per phase, each compiled for its own phase only and with its own
+// pipeline geometry (both 64-k stages in a two-slot ring: the Gram contracts
+// over K = n', up to 80 stages, and gains from the fewer barriers).
 #include "ns_common.h"
 
 namespace malt {
@@ -18,12 +19,6 @@ namespace malt {
 using namespace ns;
 
 namespace {
-
-using G = SymGeom;
-using L = SymLoads<G>;
-constexpr int BK = G::BK, STAGES = G::STAGES, H = G::H, RB = G::RB, CPR = G::CPR, RPP = G::RPP;
-constexpr int OPER_BYTES = G::OPER_BYTES, STAGE_BYTES = G::STAGE_BYTES, LOADS = G::LOADS;
-__device__ __forceinline__ int swz_rk(int row, int kc) { return G::swz_rk(row, kc); }
 
 // Epilogue staging.  A diagonal tile stages the whole bf16 tile in LDS and
 // writes it out in 512-byte rows: written column-wise (each lane: four
@@ -38,18 +33,28 @@ constexpr int ST_PITCH_R = NS_TILE * 2 + 64;
 constexpr int SYM_PITCH_T = TM * 2 + 8;
 constexpr int SYM_WAVE = TN * SYM_PITCH_T > TM * TN * 2 ? TN * SYM_PITCH_T : TM * TN * 2;
 constexpr int SYM_EPI_BYTES = NS_TILE * ST_PITCH_R;
-constexpr int LDS_BYTES = G::RING_BYTES > SYM_EPI_BYTES ? G::RING_BYTES : SYM_EPI_BYTES;
-static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
-static_assert(NW * SYM_WAVE <= LDS_BYTES, "per-wave epilogue regions");
+template <class G>
+struct SymLds {
+  static constexpr int BYTES = G::RING_BYTES > SYM_EPI_BYTES ? G::RING_BYTES : SYM_EPI_BYTES;
+  static_assert(BYTES <= 160 * 1024, "LDS budget");
+  static_assert(NW * SYM_WAVE <= BYTES, "per-wave epilogue regions");
+};
 
 }  // namespace
 
 // ===========================================================================
 // Gram and polynomial phases: C = P Q^T, symmetric output, upper tiles.
 // ===========================================================================
+// G is the stage geometry of the phase's pipeline (SymGeom for the Gram,
+// PolyGeom for the polynomial), PHASE the phase.
+template <class G, int PHASE>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
 void ns_gemm_sym_kernel(NsArgs args) {
+  using L = SymLoads<G>;
+  constexpr int BK = G::BK, STAGES = G::STAGES, H = G::H;
+  constexpr int OPER_BYTES = G::OPER_BYTES, STAGE_BYTES = G::STAGE_BYTES, LOADS = G::LOADS;
   constexpr int I = TM / 32, J = TN / 32;    // 32x32 blocks per wave
+  auto swz_rk = [](int row, int kc) { return G::swz_rk(row, kc); };
 
   extern __shared__ __attribute__((aligned(16))) char lds[];
   // Every descriptor field the tile needs is read here, before any store, so
@@ -59,7 +64,7 @@ void ns_gemm_sym_kernel(NsArgs args) {
   const Tile t = args.tiles[blockIdx.x];
   if (t.mat < 0) return;
   const MatDesc* __restrict__ d = args.desc + t.mat;
-  const int phase = args.phase;
+  constexpr int phase = PHASE;
   const int mp = d->mp, np = d->np;
   const bool split = d->split != 0;
   bf16_t* const Am = d->A;
@@ -361,12 +366,15 @@ void ns_gemm_sym_kernel(NsArgs args) {
 }
 
 
-// The kernel uses more dynamic LDS than the default limit; the attribute is
+// The kernels use more dynamic LDS than the default limit; the attribute is
 // set for the current device (plan set-up calls ns_gemm_setup with the plan's
 // device current, so every device a plan runs on has it).
 hipError_t ns_gemm_setup() {
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&ns_gemm_sym_kernel),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&ns_gemm_sym_kernel<SymGeom, PH_GRAM>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, SymLds<SymGeom>::BYTES);
+  if (e == hipSuccess)
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&ns_gemm_sym_kernel<PolyGeom, PH_POLY>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, SymLds<PolyGeom>::BYTES);
   if (e == hipSuccess) e = ns_update_setup();
   return e;
 }
@@ -374,7 +382,12 @@ hipError_t ns_gemm_setup() {
 hipError_t launch_ns_gemm(const NsArgs& a, hipStream_t s) {
   if (a.ntiles == 0) return hipSuccess;
   if (a.phase == PH_UPDATE) return launch_ns_update(a, s);
-  hipLaunchKernelGGL(ns_gemm_sym_kernel, dim3(a.ntiles), dim3(NT), LDS_BYTES, s, a);
+  if (a.phase == PH_GRAM)
+    hipLaunchKernelGGL((ns_gemm_sym_kernel<SymGeom, PH_GRAM>), dim3(a.ntiles), dim3(NT), SymLds<SymGeom>::BYTES, s,
+                       a);
+  else
+    hipLaunchKernelGGL((ns_gemm_sym_kernel<PolyGeom, PH_POLY>), dim3(a.ntiles), dim3(NT), SymLds<PolyGeom>::BYTES, s,
+                       a);
   return hipGetLastError();
 }
 
