@@ -320,6 +320,23 @@ def test_even_newton_schulz_step_counts(ns_steps):
     say(f"[parity] ns_steps={ns_steps} worst {worst}")
 
 
+@pytest.mark.parametrize("abc", [(1.5, -0.5, 0.0), (2.0, -1.5, 0.5)])
+def test_other_newton_schulz_coefficients(abc):
+    # The coefficients are hyper-parameters. c = 0 is the cubic iteration
+    # X <- a X + b X X^T X: its polynomial phase has no product, B' = a I + b A.
+    # A second quintic checks that nothing assumes Muon's numbers.
+    a, b, c = abc
+    shapes = [(300, 900), (900, 300), (768, 768), (100, 400)]
+    say(f"[parity] ns coefficients {abc} {shapes} malt x2")
+    W0 = [wl.weight(89, i, s) for i, s in enumerate(shapes)]
+    grads = [[wl.grad(89, t, i, s, "normal") for i, s in enumerate(shapes)] for t in (1, 2)]
+    hp = dict(lr=5e-3, ns_a=a, ns_b=b, ns_c=c)
+    g = run_gpu(shapes, "malt", W0, grads, hp)
+    o = run_oracle(shapes, "malt", W0, grads, hp)
+    worst = compare(g, o, "malt", label=f"ns{abc}")
+    say(f"[parity] ns coefficients {abc} worst {worst}")
+
+
 @pytest.mark.slow
 def test_c5_stress_subset_two_steps():
     # C5's two shapes at full size (4096 x 4096 and 4096 x 11008, Student-t
