@@ -75,6 +75,20 @@ __host__ __device__ constexpr int swz_kn(int k, int n) {
   return k * KN_ROW + (((n >> 3) ^ (4 * (k & 3))) << 4) + ((n & 7) << 1);
 }
 
+// Diagonal tiles of the symmetric products load one operand panel per stage
+// (their row and column panels are the same rows), half of a stage of G: the
+// same LDS ring holds twice as many of their stages, so they keep three stages
+// of loads in flight instead of one (spread between the MFMAs).
+template <class G>
+struct DiagGeom : G {
+  static constexpr int STAGES = 2 * G::STAGES;
+  static constexpr int STAGE_BYTES = G::OPER_BYTES;
+  static constexpr int RING_BYTES = STAGES * STAGE_BYTES;
+  static constexpr int LOADS = G::LOADS / 2;
+  static constexpr bool SPREAD = STAGES >= 3;
+  static_assert(RING_BYTES == G::RING_BYTES, "a diagonal tile's ring is the same LDS");
+};
+
 // The stage geometries of the kernels.
 using SymGeom = NsGeom<64, 2>;    // Gram (ns_sym.hip)
 using PolyGeom = NsGeom<64, 2>;   // polynomial (ns_sym.hip; four 32-k slots measured no faster)

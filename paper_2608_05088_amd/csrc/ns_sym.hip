@@ -122,12 +122,16 @@ void ns_gemm_sym_kernel(NsArgs args) {
   // the first half of a wave's loads are row-panel loads (SymLoads asserts it).
   // Diagonal and off-diagonal tiles run separate copies of the main loop, so
   // the block test exists only on diagonal tiles.
+  // Diagonal tiles run their own ring geometry (DiagGeom: twice the stages of
+  // half the size in the same LDS).
   auto main_loop = [&](auto diag_tag) {
     constexpr bool DIAG = decltype(diag_tag)::value;
-    pipeline<G, 1>(
-        K / BK, DIAG ? LOADS / 2 : LOADS, lds,
+    using PG = std::conditional_t<DIAG, DiagGeom<G>, G>;
+    pipeline<PG, 1>(
+        K / BK, PG::LOADS, lds,
         [&](int kt, int i) {   // diagonal tiles issue the row-panel loads q < LOADS / 2 only
-          dma16(rsP, voff[i], (uint32_t)L::soff(kt), lds_u32(lds + (kt % STAGES) * STAGE_BYTES + dst_off[i]));
+          dma16(rsP, voff[i], (uint32_t)L::soff(kt),
+                lds_u32(lds + (kt % PG::STAGES) * PG::STAGE_BYTES + dst_off[i]));
         },
         [&](int buf, const char* st, int h) {
 #pragma unroll
