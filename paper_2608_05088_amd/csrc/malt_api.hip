@@ -709,7 +709,9 @@ malt_status_t check_bounds(const Layout& L, int64_t shrink, int64_t* checked) {
           for (int lane = 0; lane < LANES; ++lane) vmax = std::max(vmax, SL::voff(g, lane, row0, col0, ld));
         return vmax + SL::soff(KT - 1) + 16;
       };
-      const uint64_t span = phase == 0 ? panel_span(ns::SymGeom{}) : panel_span(ns::PolyGeom{});
+      // A diagonal tile loads its row panel with the Gram geometry's load map.
+      const uint64_t span = diag ? panel_span(ns::SymGeom{}) : phase == 0 ? panel_span(ns::SymGeom{})
+                                                                           : panel_span(ns::PolyGeom{});
       if (!B.range(kname, phase == 0 ? "X panels" : "A panels", t, 0, span, psz, true)) return B.st;
       if (phase == 1) {
         uint64_t amax = 0;

@@ -50,11 +50,7 @@ struct SymLds {
 template <class G, int PHASE>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
 void ns_gemm_sym_kernel(NsArgs args) {
-  using L = SymLoads<G>;
-  constexpr int BK = G::BK, STAGES = G::STAGES, H = G::H;
-  constexpr int OPER_BYTES = G::OPER_BYTES, STAGE_BYTES = G::STAGE_BYTES, LOADS = G::LOADS;
   constexpr int I = TM / 32, J = TN / 32;    // 32x32 blocks per wave
-  auto swz_rk = [](int row, int kc) { return G::swz_rk(row, kc); };
 
   extern __shared__ __attribute__((aligned(16))) char lds[];
   // Every descriptor field the tile needs is read here, before any store, so
@@ -87,28 +83,6 @@ void ns_gemm_sym_kernel(NsArgs args) {
   const int role = diag ? ((0x76540132u >> (4 * wave)) & 0xF) : wave;
   const int wr = role / (NW / 2), wc = role % (NW / 2);
 
-  // Direct-load sources: load g < LOADS_PER_OPER covers rows of the tile-row
-  // panel, the rest rows of the tile-column panel (both of P); 32-bit byte
-  // offsets into P's buffer (SymLoads, shared with the host bounds check).
-  const i32x4 rsP = buf_rsrc(P);
-  uint32_t voff[LOADS];
-  int dst_off[LOADS];
-#pragma unroll
-  for (int q = 0; q < LOADS; ++q) {
-    const int g = wave + q * NW;
-    voff[q] = (uint32_t)L::voff(g, lane, row0, col0, ld);
-    dst_off[q] = L::dst(g);
-  }
-  int offa[I][H], offb[J][H];
-#pragma unroll
-  for (int h = 0; h < H; ++h) {
-    const int kc = 2 * h + (lane >> 5);
-#pragma unroll
-    for (int i = 0; i < I; ++i) offa[i][h] = swz_rk(wr * TM + i * 32 + (lane & 31), kc);
-#pragma unroll
-    for (int j = 0; j < J; ++j) offb[j][h] = (diag ? 0 : OPER_BYTES) + swz_rk(wc * TN + j * 32 + (lane & 31), kc);
-  }
-
   f32x16 acc[I][J];
 #pragma unroll
   for (int i = 0; i < I; ++i)
@@ -116,21 +90,45 @@ void ns_gemm_sym_kernel(NsArgs args) {
     for (int j = 0; j < J; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-  bf16x8 fa[2][I], fb[2][J];
+  const i32x4 rsP = buf_rsrc(P);
 
-  // With 8 waves, g = wave + 8q < LOADS_PER_OPER exactly for q < LOADS / 2:
-  // the first half of a wave's loads are row-panel loads (SymLoads asserts it).
   // Diagonal and off-diagonal tiles run separate copies of the main loop, so
-  // the block test exists only on diagonal tiles.
-  // Diagonal tiles run their own ring geometry (DiagGeom: twice the stages of
-  // half the size in the same LDS).
+  // the block test exists only on diagonal tiles, and each has its own ring
+  // geometry: G for off-diagonal tiles, DiagGeom<SymGeom> (64-k stages of the
+  // row panel alone, four in the ring) for diagonal ones.
   auto main_loop = [&](auto diag_tag) {
     constexpr bool DIAG = decltype(diag_tag)::value;
-    using PG = std::conditional_t<DIAG, DiagGeom<G>, G>;
+    using PG = std::conditional_t<DIAG, DiagGeom<SymGeom>, G>;
+    using PL = SymLoads<std::conditional_t<DIAG, SymGeom, G>>;
+    constexpr int H = PG::H, NL = PG::LOADS;
+    // Direct-load sources: load g < LOADS_PER_OPER covers rows of the tile-row
+    // panel, the rest rows of the tile-column panel (both of P); 32-bit byte
+    // offsets into P's buffer (SymLoads, shared with the host bounds check).
+    // With 8 waves, g = wave + 8q < LOADS_PER_OPER exactly for q < LOADS / 2:
+    // the first half of a wave's loads are row-panel loads (SymLoads asserts
+    // it), and a diagonal tile issues those only.
+    uint32_t voff[NL];
+    int dst_off[NL];
+#pragma unroll
+    for (int q = 0; q < NL; ++q) {
+      const int g = wave + q * NW;
+      voff[q] = (uint32_t)PL::voff(g, lane, row0, col0, ld);
+      dst_off[q] = PL::dst(g);
+    }
+    int offa[I][H], offb[J][H];
+#pragma unroll
+    for (int h = 0; h < H; ++h) {
+      const int kc = 2 * h + (lane >> 5);
+#pragma unroll
+      for (int i = 0; i < I; ++i) offa[i][h] = PG::swz_rk(wr * TM + i * 32 + (lane & 31), kc);
+#pragma unroll
+      for (int j = 0; j < J; ++j) offb[j][h] = (DIAG ? 0 : PG::OPER_BYTES) + PG::swz_rk(wc * TN + j * 32 + (lane & 31), kc);
+    }
+    bf16x8 fa[2][I], fb[2][J];
     pipeline<PG, 1>(
-        K / BK, PG::LOADS, lds,
-        [&](int kt, int i) {   // diagonal tiles issue the row-panel loads q < LOADS / 2 only
-          dma16(rsP, voff[i], (uint32_t)L::soff(kt),
+        K / PG::BK, NL, lds,
+        [&](int kt, int i) {
+          dma16(rsP, voff[i], (uint32_t)PL::soff(kt),
                 lds_u32(lds + (kt % PG::STAGES) * PG::STAGE_BYTES + dst_off[i]));
         },
         [&](int buf, const char* st, int h) {
