@@ -505,19 +505,8 @@ __global__ __launch_bounds__(EW_THREADS) void backmap_write_kernel(EwArgs a) {
   MALT_GLOBAL float* __restrict__ W = gptr(a.ptrs[t.mat].W);
   const float coef = (float)gptr(d.scal)[SC_COEF];
   const float decay = a.decay;
-  if (d.tall) {
-    // Canonical rows c0 .. c0+255 (W columns), columns r0 .. r0+31 (W rows):
-    // four threads per canonical row, 16 bytes (four words) each, inside the
-    // padded buffer.
-    const int cr = threadIdx.x >> 2, q = threadIdx.x & 3;
-    const ew_u32x4 v =
-        __builtin_nontemporal_load(reinterpret_cast<const MALT_GLOBAL ew_u32x4*>(O + (size_t)(c0 + cr) * ldo + r0 + q * 8));
-    osh[bm_word(cr, 4 * q + 0)] = v.x;
-    osh[bm_word(cr, 4 * q + 1)] = v.y;
-    osh[bm_word(cr, 4 * q + 2)] = v.z;
-    osh[bm_word(cr, 4 * q + 3)] = v.w;
-    __syncthreads();
-  }
+  // Every global load is issued before the tall path's LDS staging and its
+  // barrier, so W's loads are in flight while O's block makes its round trip.
   float Rv[4];
   load4(gptr(d.Rv), c, n, true, Rv);
   const int rw = r0 + w * RPW;   // this wave's first row
@@ -532,6 +521,19 @@ __global__ __launch_bounds__(EW_THREADS) void backmap_write_kernel(EwArgs a) {
         pk[u] = make_uint2(q.x, q.y);
       }
     }
+  }
+  if (d.tall) {
+    // Canonical rows c0 .. c0+255 (W columns), columns r0 .. r0+31 (W rows):
+    // four threads per canonical row, 16 bytes (four words) each, inside the
+    // padded buffer.
+    const int cr = threadIdx.x >> 2, q = threadIdx.x & 3;
+    const ew_u32x4 v =
+        __builtin_nontemporal_load(reinterpret_cast<const MALT_GLOBAL ew_u32x4*>(O + (size_t)(c0 + cr) * ldo + r0 + q * 8));
+    osh[bm_word(cr, 4 * q + 0)] = v.x;
+    osh[bm_word(cr, 4 * q + 1)] = v.y;
+    osh[bm_word(cr, 4 * q + 2)] = v.z;
+    osh[bm_word(cr, 4 * q + 3)] = v.w;
+    __syncthreads();
   }
   uint32_t ow[4];   // tall: W rows rw, rw + 1 at W column c + e
   if (d.tall) {
