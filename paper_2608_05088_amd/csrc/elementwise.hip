@@ -32,9 +32,11 @@ typedef unsigned ew_u32x4 __attribute__((ext_vector_type(4)));
 
 // Load 4 consecutive floats of one row starting at column c (columns >= n
 // read 0). STREAM marks data this step reads once (non-temporal load).
-template <bool STREAM = false>
+// INSIDE: the caller has established that the row allows 16-byte access and
+// c + 3 < n, so the load is unconditional.
+template <bool STREAM = false, bool INSIDE = false>
 __device__ __forceinline__ void load4(const MALT_GLOBAL float* __restrict__ p, int c, int n, bool vec, float v[4]) {
-  if (vec && c + 3 < n) {
+  if (INSIDE || (vec && c + 3 < n)) {
     ew_f32x4 x;
     if (STREAM) x = __builtin_nontemporal_load(reinterpret_cast<const MALT_GLOBAL ew_f32x4*>(p + c));
     else x = *reinterpret_cast<const MALT_GLOBAL ew_f32x4*>(p + c);
@@ -45,8 +47,9 @@ __device__ __forceinline__ void load4(const MALT_GLOBAL float* __restrict__ p, i
   }
 }
 
+template <bool INSIDE = false>
 __device__ __forceinline__ void store4(MALT_GLOBAL float* __restrict__ p, int c, int n, bool vec, const float v[4]) {
-  if (vec && c + 3 < n) {
+  if (INSIDE || (vec && c + 3 < n)) {
     const ew_f32x4 x = {v[0], v[1], v[2], v[3]};
     *reinterpret_cast<MALT_GLOBAL ew_f32x4*>(p + c) = x;
   } else {
@@ -56,37 +59,84 @@ __device__ __forceinline__ void store4(MALT_GLOBAL float* __restrict__ p, int c,
   }
 }
 
+// One matrix's descriptor fields and caller pointers, as the tile passes use
+// them, read in one place before any branch: the compiler then issues them as
+// one batch of scalar loads, not a chain of load-and-wait behind each test.
+struct EwView {
+  int m, n, np, tall;
+  bool vec;
+  MALT_GLOBAL float* W;
+  const MALT_GLOBAL float* G;
+  MALT_GLOBAL float* M;
+  const MALT_GLOBAL float* Lv;
+  const MALT_GLOBAL float* Rv;
+  MALT_GLOBAL float* rowpart;
+  MALT_GLOBAL float* colpart;
+  MALT_GLOBAL float* k2part;
+  MALT_GLOBAL bf16_t* X0;
+  const MALT_GLOBAL bf16_t* O;   // back-map: the buffer holding the final iterate
+  const MALT_GLOBAL double* scal;
+};
+
+__device__ __forceinline__ EwView ew_view(const EwArgs& a, int mat) {
+  const MatDesc& d = a.desc[mat];
+  const PtrPair& p = a.ptrs[mat];
+  EwView v;
+  v.m = d.m;
+  v.n = d.n;
+  v.np = d.np;
+  v.tall = d.tall;
+  v.vec = p.vec != 0;
+  v.W = gptr(p.W);
+  v.G = gptr(p.G);
+  v.M = gptr(d.M);
+  v.Lv = gptr(d.Lv);
+  v.Rv = gptr(d.Rv);
+  v.rowpart = gptr(d.rowpart);
+  v.colpart = gptr(d.colpart);
+  v.k2part = gptr(d.k2part);
+  v.X0 = gptr(d.X[0]);
+  v.O = gptr(d.X[a.o_parity]);
+  v.scal = gptr(d.scal);
+  return v;
+}
+
 // ---------------------------------------------------------------------------
 // Momentum EMA (Alg. 1/2, momentum line) fused with the per-tile row and
 // column sums of G^2 that feed the l, r EMAs (Eq. dp_preconditioner).
 // Reads G and M, writes M: 12 bytes per element.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(EW_THREADS) void momentum_rowcol_kernel(EwArgs a) {
+// Interior tiles (every row and column of the tile inside the matrix, rows
+// open to 16-byte access) take INSIDE = true: no bounds test anywhere, so
+// each lane's loads form one straight run and are all in flight together.
+// (With a bounds branch per row the compiler waited for one row's loads
+// before issuing the next row's.)  Edge tiles take the checked path.
+template <bool INSIDE>
+__device__ __forceinline__ void momentum_tile(const EwArgs& a, const EwView& v, const Tile& t, float (*colsh)[EW_TC]) {
   constexpr int NW = EW_THREADS / 64, RPW = EW_TR / NW;   // 16 waves, 2 rows each
   static_assert(NW * RPW == EW_TR && EW_TC == 256, "one 256-column row segment per wave and row");
-  __shared__ float colsh[NW][EW_TC];
-  const Tile t = a.tiles[xcd_remap(blockIdx.x, gridDim.x)];
-  const MatDesc& d = a.desc[t.mat];
-  const int m = d.m, n = d.n;
-  const bool vec = a.ptrs[t.mat].vec != 0;
+  const int m = v.m, n = v.n;
+  const bool vec = v.vec;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int r0 = t.ti * EW_TR + w * RPW, c = t.tj * EW_TC + lane * 4;
-  const MALT_GLOBAL float* __restrict__ G = gptr(a.ptrs[t.mat].G);
-  MALT_GLOBAL float* __restrict__ M = gptr(d.M);
+  const MALT_GLOBAL float* __restrict__ G = v.G;
+  MALT_GLOBAL float* __restrict__ M = v.M;
+  MALT_GLOBAL float* __restrict__ rowpart = v.rowpart;
+  MALT_GLOBAL float* __restrict__ colpart = v.colpart;
   float g[RPW][4], mm[RPW][4];
 #pragma unroll
   for (int u = 0; u < RPW; ++u) {
-    if (r0 + u < m) {
+    if (INSIDE || r0 + u < m) {
       const size_t off = (size_t)(r0 + u) * n;
-      load4<true>(G + off, c, n, vec, g[u]);
-      load4(M + off, c, n, vec, mm[u]);
+      load4<true, INSIDE>(G + off, c, n, vec, g[u]);
+      load4<false, INSIDE>(M + off, c, n, vec, mm[u]);
     }
   }
   float cacc[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int u = 0; u < RPW; ++u) {
     const int r = r0 + u;
-    if (r >= m) break;   // uniform over the wave
+    if (!INSIDE && r >= m) break;   // uniform over the wave
     float racc = 0.f;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -95,21 +145,30 @@ __global__ __launch_bounds__(EW_THREADS) void momentum_rowcol_kernel(EwArgs a) {
       racc += g2;
       cacc[e] += g2;
     }
-    store4(M + (size_t)r * n, c, n, vec, mm[u]);
+    store4<INSIDE>(M + (size_t)r * n, c, n, vec, mm[u]);
     racc = wave_sum(racc);
-    if (lane == 0) gptr(d.rowpart)[(size_t)t.tj * m + r] = racc;
+    if (lane == 0) rowpart[(size_t)t.tj * m + r] = racc;
   }
 #pragma unroll
   for (int e = 0; e < 4; ++e) colsh[w][lane * 4 + e] = cacc[e];
   __syncthreads();
   const int cc = threadIdx.x;
   const int col = t.tj * EW_TC + cc;
-  if (cc < EW_TC && col < n) {
+  if (cc < EW_TC && (INSIDE || col < n)) {
     float s = 0.f;
 #pragma unroll
     for (int k = 0; k < NW; ++k) s += colsh[k][cc];
-    gptr(d.colpart)[(size_t)t.ti * n + col] = s;
+    colpart[(size_t)t.ti * n + col] = s;
   }
+}
+
+__global__ __launch_bounds__(EW_THREADS) void momentum_rowcol_kernel(EwArgs a) {
+  __shared__ float colsh[EW_THREADS / 64][EW_TC];
+  const Tile t = a.tiles[xcd_remap(blockIdx.x, gridDim.x)];
+  const EwView v = ew_view(a, t.mat);
+  const bool inside = v.vec & ((t.ti + 1) * EW_TR <= v.m) & ((t.tj + 1) * EW_TC <= v.n);
+  if (inside) momentum_tile<true>(a, v, t, colsh);
+  else momentum_tile<false>(a, v, t, colsh);
 }
 
 // ---------------------------------------------------------------------------
@@ -161,33 +220,40 @@ __global__ __launch_bounds__(NTHREADS) void precond_finalize_kernel(EwArgs a) {
 // Wide matrices: the canonical matrix is W. Tiles of K2W_R padded rows x
 // EW_TC padded columns; each wave converts K2W_R / waves consecutive rows, one
 // float4 of M (and of G) per lane and row, all loads issued first.
-template <bool MALTER>
-__global__ __launch_bounds__(K2W_THREADS) void scale_convert_wide_kernel(EwArgs a) {
+// Interior tiles (INSIDE: all K2W_R rows and EW_TC columns inside W, 16-byte
+// rows) load without bounds tests, as in the momentum pass.
+template <bool MALTER, bool INSIDE>
+__device__ __forceinline__ void scale_convert_wide_tile(const EwView& v, const Tile& t, float (*red)[K2W_THREADS / 64]) {
   constexpr int NW = K2W_THREADS / 64, RPW = K2W_R / NW;
   static_assert(NW * RPW == K2W_R && EW_TC == 256, "whole 256-column row segments per wave");
-  __shared__ float red[2][NW];
-  const Tile t = a.tiles[xcd_remap(blockIdx.x, gridDim.x)];
-  const MatDesc& d = a.desc[t.mat];
-  const int m = d.m, n = d.n;
-  const bool vec = a.ptrs[t.mat].vec != 0;
+  const int m = v.m, n = v.n;
+  const bool vec = v.vec;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int rw = t.ti * K2W_R + w * RPW, c = t.tj * EW_TC + lane * 4;   // rows < mp, c < np
+  const MALT_GLOBAL float* __restrict__ M = v.M;
+  const MALT_GLOBAL float* __restrict__ G = v.G;
+  const MALT_GLOBAL float* __restrict__ Lv = v.Lv;
+  MALT_GLOBAL bf16_t* __restrict__ X0 = v.X0;
+  const int ldx = v.np;
   float mm[RPW][4], gg[RPW][4], rv[4];
 #pragma unroll
   for (int u = 0; u < RPW; ++u) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) mm[u][e] = gg[u][e] = 0.f;
-    if (rw + u < m) {
-      load4(gptr(d.M) + (size_t)(rw + u) * n, c, n, vec, mm[u]);
-      if (MALTER) load4(gptr(a.ptrs[t.mat].G) + (size_t)(rw + u) * n, c, n, vec, gg[u]);
+    if (INSIDE || rw + u < m) {
+      load4<false, INSIDE>(M + (size_t)(rw + u) * n, c, n, vec, mm[u]);
+      if (MALTER) load4<false, INSIDE>(G + (size_t)(rw + u) * n, c, n, vec, gg[u]);
     }
   }
-  load4(gptr(d.Rv), c, n, true, rv);
+  load4<false, INSIDE>(v.Rv, c, n, true, rv);
+  float lv[RPW];   // all read before the first store, which the compiler cannot tell apart from Lv
+#pragma unroll
+  for (int u = 0; u < RPW; ++u) lv[u] = (INSIDE || rw + u < m) ? Lv[rw + u] : 0.f;
   float s2 = 0.f, q2 = 0.f;
 #pragma unroll
   for (int u = 0; u < RPW; ++u) {
     const int r = rw + u;
-    const float li = r < m ? gptr(d.Lv)[r] : 0.f;
+    const float li = lv[u];
     float x[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -200,7 +266,7 @@ __global__ __launch_bounds__(K2W_THREADS) void scale_convert_wide_kernel(EwArgs 
     }
     // X0 is consumed by the next kernel from L2/HBM; streaming store.
     const ew_u32x2 pk = {pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3])};
-    __builtin_nontemporal_store(pk, reinterpret_cast<MALT_GLOBAL ew_u32x2*>(gptr(d.X[0]) + (size_t)r * d.np + c));
+    __builtin_nontemporal_store(pk, reinterpret_cast<MALT_GLOBAL ew_u32x2*>(X0 + (size_t)r * ldx + c));
   }
   s2 = wave_sum(s2);
   if (MALTER) q2 = wave_sum(q2);
@@ -216,9 +282,19 @@ __global__ __launch_bounds__(K2W_THREADS) void scale_convert_wide_kernel(EwArgs 
       so += red[0][k];
       sq += red[1][k];
     }
-    gptr(d.k2part)[2 * (size_t)t.idx + 0] = so;
-    gptr(d.k2part)[2 * (size_t)t.idx + 1] = sq;
+    v.k2part[2 * (size_t)t.idx + 0] = so;
+    v.k2part[2 * (size_t)t.idx + 1] = sq;
   }
+}
+
+template <bool MALTER>
+__global__ __launch_bounds__(K2W_THREADS) void scale_convert_wide_kernel(EwArgs a) {
+  __shared__ float red[2][K2W_THREADS / 64];
+  const Tile t = a.tiles[xcd_remap(blockIdx.x, gridDim.x)];
+  const EwView v = ew_view(a, t.mat);
+  const bool inside = v.vec & ((t.ti + 1) * K2W_R <= v.m) & ((t.tj + 1) * EW_TC <= v.n);
+  if (inside) scale_convert_wide_tile<MALTER, true>(v, t, red);
+  else scale_convert_wide_tile<MALTER, false>(v, t, red);
 }
 
 // Tall matrices: the canonical matrix is W^T, written through an LDS
@@ -236,8 +312,11 @@ __global__ __launch_bounds__(K2W_THREADS) void scale_convert_wide_kernel(EwArgs 
 // pieces.
 __device__ __forceinline__ int tall_word(int c, int p) { return c * (K2_T / 2) + ((p + 2 * (c >> 2) + (c & 3)) & (K2_T / 2 - 1)); }
 
-template <bool MALTER>
-__global__ __launch_bounds__(K2T_THREADS) void scale_convert_tall_kernel(EwArgs a) {
+// Interior groups (INSIDE: the 64 W rows and TG * 64 W columns inside W,
+// 16-byte rows) load without bounds tests, as in the momentum pass.
+template <bool MALTER, bool INSIDE>
+__device__ __forceinline__ void scale_convert_tall_group(const EwView& v, const Tile& t, uint32_t (*tsh)[K2_T * (K2_T / 2)],
+                                                         float (*red)[K2T_THREADS / 64]) {
   constexpr int TG = K2_GROUP;
   constexpr int NW = K2T_THREADS / 64;
   constexpr int NP = K2T_THREADS / 16;         // row pairs per pass: 16 threads x 4 columns span 64 columns
@@ -247,17 +326,12 @@ __global__ __launch_bounds__(K2T_THREADS) void scale_convert_tall_kernel(EwArgs 
   constexpr int ROWS_OUT = K2T_THREADS / CPR;  // canonical rows per copy-out pass
   static_assert(PASSES * 2 * NP == K2_T && K2_T % ROWS_OUT == 0, "tall tile layout");
   static_assert(WPR == 32, "tall_word rotates within 32-word rows");
-  __shared__ uint32_t tsh[TG][K2_T * WPR];
-  __shared__ float red[2 * TG][NW];
-  const int grp = xcd_remap(blockIdx.x, gridDim.x);
-  const Tile t = a.tiles[grp * TG];
-  const MatDesc& d = a.desc[t.mat];
-  const int m = d.m, n = d.n;
-  const bool vec = a.ptrs[t.mat].vec != 0;
-  MALT_GLOBAL bf16_t* __restrict__ X0 = gptr(d.X[0]);
-  const int ldx = d.np;                  // canonical row pitch
-  const MALT_GLOBAL float* __restrict__ M = gptr(d.M);
-  const MALT_GLOBAL float* __restrict__ G = gptr(a.ptrs[t.mat].G);
+  const int m = v.m, n = v.n;
+  const bool vec = v.vec;
+  MALT_GLOBAL bf16_t* __restrict__ X0 = v.X0;
+  const int ldx = v.np;                  // canonical row pitch
+  const MALT_GLOBAL float* __restrict__ M = v.M;
+  const MALT_GLOBAL float* __restrict__ G = v.G;
   const int r0 = t.ti * K2_T, cb = t.tj * K2_T;   // band columns cb .. cb + TG*K2_T
   const int cg = threadIdx.x & 15;                // W columns 4 cg .. 4 cg + 3 of each tile
   const int pp = threadIdx.x >> 4;                // row pair pp + NP * pass
@@ -268,7 +342,7 @@ __global__ __launch_bounds__(K2T_THREADS) void scale_convert_tall_kernel(EwArgs 
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int r = r0 + 2 * (pp + NP * ps) + u;
-      Li[ps][u] = r < m ? gptr(d.Lv)[r] : 0.f;
+      Li[ps][u] = (INSIDE || r < m) ? v.Lv[r] : 0.f;
     }
   float Rv[TG][4];
 #pragma unroll
@@ -276,7 +350,7 @@ __global__ __launch_bounds__(K2T_THREADS) void scale_convert_tall_kernel(EwArgs 
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int c = cb + j * K2_T + 4 * cg + e;
-      Rv[j][e] = c < n ? gptr(d.Rv)[c] : 0.f;
+      Rv[j][e] = (INSIDE || c < n) ? v.Rv[c] : 0.f;
     }
   float mm[TG][PASSES][2][4], gg[TG][PASSES][2][4];
 #pragma unroll
@@ -289,9 +363,9 @@ __global__ __launch_bounds__(K2T_THREADS) void scale_convert_tall_kernel(EwArgs 
         const int c = cb + j * K2_T + 4 * cg;
 #pragma unroll
         for (int e = 0; e < 4; ++e) mm[j][ps][u][e] = gg[j][ps][u][e] = 0.f;
-        if (r < m) {
-          load4(M + (size_t)r * n, c, n, vec, mm[j][ps][u]);
-          if (MALTER) load4(G + (size_t)r * n, c, n, vec, gg[j][ps][u]);
+        if (INSIDE || r < m) {
+          load4<false, INSIDE>(M + (size_t)r * n, c, n, vec, mm[j][ps][u]);
+          if (MALTER) load4<false, INSIDE>(G + (size_t)r * n, c, n, vec, gg[j][ps][u]);
         }
       }
 
@@ -326,10 +400,10 @@ __global__ __launch_bounds__(K2T_THREADS) void scale_convert_tall_kernel(EwArgs 
   for (int j = 0; j < TG; ++j)
 #pragma unroll
     for (int rr = threadIdx.x / CPR; rr < K2_T; rr += ROWS_OUT) {
-      const ew_u32x4 v = {tsh[j][tall_word(rr, 4 * piece + 0)], tsh[j][tall_word(rr, 4 * piece + 1)],
+      const ew_u32x4 wv = {tsh[j][tall_word(rr, 4 * piece + 0)], tsh[j][tall_word(rr, 4 * piece + 1)],
                           tsh[j][tall_word(rr, 4 * piece + 2)], tsh[j][tall_word(rr, 4 * piece + 3)]};
       __builtin_nontemporal_store(
-          v, reinterpret_cast<MALT_GLOBAL ew_u32x4*>(X0 + (size_t)(cb + j * K2_T + rr) * ldx + r0 + 8 * piece));
+          wv, reinterpret_cast<MALT_GLOBAL ew_u32x4*>(X0 + (size_t)(cb + j * K2_T + rr) * ldx + r0 + 8 * piece));
     }
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
 #pragma unroll
@@ -350,9 +424,21 @@ __global__ __launch_bounds__(K2T_THREADS) void scale_convert_tall_kernel(EwArgs 
       so += red[2 * j][k];
       sq += red[2 * j + 1][k];
     }
-    gptr(d.k2part)[2 * (size_t)(t.idx + j) + 0] = so;
-    gptr(d.k2part)[2 * (size_t)(t.idx + j) + 1] = sq;
+    v.k2part[2 * (size_t)(t.idx + j) + 0] = so;
+    v.k2part[2 * (size_t)(t.idx + j) + 1] = sq;
   }
+}
+
+
+template <bool MALTER>
+__global__ __launch_bounds__(K2T_THREADS) void scale_convert_tall_kernel(EwArgs a) {
+  __shared__ uint32_t tsh[K2_GROUP][K2_T * (K2_T / 2)];
+  __shared__ float red[2 * K2_GROUP][K2T_THREADS / 64];
+  const Tile t = a.tiles[xcd_remap(blockIdx.x, gridDim.x) * K2_GROUP];
+  const EwView v = ew_view(a, t.mat);
+  const bool inside = v.vec & ((t.ti + 1) * K2_T <= v.m) & ((t.tj + K2_GROUP) * K2_T <= v.n);
+  if (inside) scale_convert_tall_group<MALTER, true>(v, t, tsh, red);
+  else scale_convert_tall_group<MALTER, false>(v, t, tsh, red);
 }
 
 // Fixed-order block reduction of count pairs (stride 2) into float64 sums.
@@ -489,64 +575,69 @@ __device__ __forceinline__ int bm_word(int c, int w) {
   return w * EW_TC + e * 64 + ((l + 8 * e + 2 * (w >> 2)) & 63);
 }
 
-__global__ __launch_bounds__(EW_THREADS) void backmap_write_kernel(EwArgs a) {
+// Instances per orientation (TALL) and per interior tile (INSIDE: all EW_TR
+// rows and EW_TC columns inside W, 16-byte rows; no bounds tests, as in the
+// momentum pass). Every global load is issued before the tall path's LDS
+// staging and its barrier, so W's loads are in flight while O's block makes
+// its round trip.
+template <bool TALL, bool INSIDE>
+__device__ __forceinline__ void backmap_tile(const EwArgs& a, const EwView& v, const Tile& t, uint32_t* osh) {
   constexpr int NW = EW_THREADS / 64, RPW = EW_TR / NW;   // 16 waves, 2 rows each
   static_assert(NW * RPW == EW_TR && EW_TC * EW_TR == EW_THREADS * 8, "tall fill: 8 bf16 per thread");
   static_assert(RPW == 2 && EW_TC == 256, "tall read: one word holds a wave's two rows; 64 lanes x 4 columns");
-  __shared__ uint32_t osh[EW_TR / 2 * EW_TC];   // tall: O^T block as words (see bm_word)
-  const Tile t = a.tiles[xcd_remap(blockIdx.x, gridDim.x)];
-  const MatDesc& d = a.desc[t.mat];
-  const int m = d.m, n = d.n;
-  const bool vec = a.ptrs[t.mat].vec != 0;
+  const int m = v.m, n = v.n;
+  const bool vec = v.vec;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int r0 = t.ti * EW_TR, c0 = t.tj * EW_TC, c = c0 + lane * 4;
-  const MALT_GLOBAL bf16_t* __restrict__ O = gptr(d.X[a.o_parity]);
-  const int ldo = d.np;
-  MALT_GLOBAL float* __restrict__ W = gptr(a.ptrs[t.mat].W);
-  const float coef = (float)gptr(d.scal)[SC_COEF];
-  const float decay = a.decay;
-  // Every global load is issued before the tall path's LDS staging and its
-  // barrier, so W's loads are in flight while O's block makes its round trip.
-  float Rv[4];
-  load4(gptr(d.Rv), c, n, true, Rv);
+  const MALT_GLOBAL bf16_t* __restrict__ O = v.O;
+  const int ldo = v.np;
+  MALT_GLOBAL float* __restrict__ W = v.W;
+  const MALT_GLOBAL float* __restrict__ Lv = v.Lv;
   const int rw = r0 + w * RPW;   // this wave's first row
   float wv[RPW][4];
   uint2 pk[RPW];
 #pragma unroll
   for (int u = 0; u < RPW; ++u) {
-    if (rw + u < m) {
-      load4(W + (size_t)(rw + u) * n, c, n, vec, wv[u]);
-      if (!d.tall) {
+    if (INSIDE || rw + u < m) {
+      load4<false, INSIDE>(W + (size_t)(rw + u) * n, c, n, vec, wv[u]);
+      if (!TALL) {
         const ew_u32x2 q = __builtin_nontemporal_load(reinterpret_cast<const MALT_GLOBAL ew_u32x2*>(O + (size_t)(rw + u) * ldo + c));
         pk[u] = make_uint2(q.x, q.y);
       }
     }
   }
-  if (d.tall) {
+  ew_u32x4 ob;
+  const int cr = threadIdx.x >> 2, q = threadIdx.x & 3;
+  if (TALL) {
     // Canonical rows c0 .. c0+255 (W columns), columns r0 .. r0+31 (W rows):
     // four threads per canonical row, 16 bytes (four words) each, inside the
     // padded buffer.
-    const int cr = threadIdx.x >> 2, q = threadIdx.x & 3;
-    const ew_u32x4 v =
-        __builtin_nontemporal_load(reinterpret_cast<const MALT_GLOBAL ew_u32x4*>(O + (size_t)(c0 + cr) * ldo + r0 + q * 8));
-    osh[bm_word(cr, 4 * q + 0)] = v.x;
-    osh[bm_word(cr, 4 * q + 1)] = v.y;
-    osh[bm_word(cr, 4 * q + 2)] = v.z;
-    osh[bm_word(cr, 4 * q + 3)] = v.w;
-    __syncthreads();
+    ob = __builtin_nontemporal_load(reinterpret_cast<const MALT_GLOBAL ew_u32x4*>(O + (size_t)(c0 + cr) * ldo + r0 + q * 8));
   }
+  float Rv[4];
+  load4<false, INSIDE>(v.Rv, c, n, true, Rv);
+  const float coef = (float)v.scal[SC_COEF];
+  const float decay = a.decay;
+  float lv[RPW];   // all read before the first store, which the compiler cannot tell apart from Lv
+#pragma unroll
+  for (int u = 0; u < RPW; ++u) lv[u] = (INSIDE || rw + u < m) ? Lv[rw + u] : 0.f;
   uint32_t ow[4];   // tall: W rows rw, rw + 1 at W column c + e
-  if (d.tall) {
+  if (TALL) {
+    osh[bm_word(cr, 4 * q + 0)] = ob.x;
+    osh[bm_word(cr, 4 * q + 1)] = ob.y;
+    osh[bm_word(cr, 4 * q + 2)] = ob.z;
+    osh[bm_word(cr, 4 * q + 3)] = ob.w;
+    __syncthreads();
 #pragma unroll
     for (int e = 0; e < 4; ++e) ow[e] = osh[bm_word(4 * lane + e, w)];
   }
 #pragma unroll
   for (int u = 0; u < RPW; ++u) {
     const int r = rw + u;
-    if (r >= m) break;   // uniform over the wave
-    const float cl = coef * gptr(d.Lv)[r];
+    if (!INSIDE && r >= m) break;   // uniform over the wave
+    const float cl = coef * lv[u];
     float o[4];
-    if (!d.tall) {
+    if (!TALL) {
       o[0] = bf16_lo(pk[u].x);
       o[1] = bf16_hi(pk[u].x);
       o[2] = bf16_lo(pk[u].y);
@@ -557,7 +648,21 @@ __global__ __launch_bounds__(EW_THREADS) void backmap_write_kernel(EwArgs a) {
     }
 #pragma unroll
     for (int e = 0; e < 4; ++e) wv[u][e] = decay * wv[u][e] - cl * o[e] * Rv[e];
-    store4(W + (size_t)r * n, c, n, vec, wv[u]);
+    store4<INSIDE>(W + (size_t)r * n, c, n, vec, wv[u]);
+  }
+}
+
+__global__ __launch_bounds__(EW_THREADS) void backmap_write_kernel(EwArgs a) {
+  __shared__ uint32_t osh[EW_TR / 2 * EW_TC];   // tall: O^T block as words (see bm_word)
+  const Tile t = a.tiles[xcd_remap(blockIdx.x, gridDim.x)];
+  const EwView v = ew_view(a, t.mat);
+  const bool inside = v.vec & ((t.ti + 1) * EW_TR <= v.m) & ((t.tj + 1) * EW_TC <= v.n);
+  if (v.tall) {
+    if (inside) backmap_tile<true, true>(a, v, t, osh);
+    else backmap_tile<true, false>(a, v, t, osh);
+  } else {
+    if (inside) backmap_tile<false, true>(a, v, t, osh);
+    else backmap_tile<false, false>(a, v, t, osh);
   }
 }
 
