@@ -26,6 +26,7 @@ namespace ns {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
@@ -36,16 +37,21 @@ constexpr int NT = NW * 64;                 // threads per workgroup
 constexpr int KN_ROW = NS_TILE * 2;         // bytes per [k][n] tile row (512)
 // Wave grid 2 x (NW / 2): each wave owns TM x TN of the 256 x 256 tile.
 constexpr int TM = NS_TILE / 2, TN = NS_TILE / (NW / 2);
-constexpr int NMMA = (TM / 32) * (TN / 32);   // MFMAs per wave per 16-k sub-step
 static_assert(TM == 128 && TN == 64, "the epilogues assume 128 x 64 wave sub-tiles");
 
 // Stage geometry of one kernel's pipeline: BK k-values per stage, a ring of
-// STAGES stage slots in LDS.
-template <int BK_, int STAGES_>
+// STAGES stage slots in LDS, sub-steps of KSUB k-values, one MFMA k-step: 16
+// for v_mfma_f32_32x32x16_bf16 (32 x 32 blocks), 32 for
+// v_mfma_f32_16x16x32_bf16 (16 x 16 blocks).
+template <int BK_, int STAGES_, int KSUB_ = 16>
 struct NsGeom {
   static constexpr int BK = BK_;
   static constexpr int STAGES = STAGES_;
-  static constexpr int H = BK / 16;                           // MFMA sub-steps per stage
+  static constexpr int KSUB = KSUB_;
+  static constexpr int H = BK / KSUB;                         // MFMA sub-steps per stage
+  static constexpr int BLK = KSUB == 16 ? 32 : 16;            // output block edge of one MFMA
+  static constexpr int NMMA = (TM / BLK) * (TN / BLK);        // MFMAs per wave per sub-step
+  static_assert(KSUB == 16 || KSUB == 32, "the two bf16 MFMA shapes");
   static constexpr int RB = BK * 2;                           // bytes per [row][k] tile row
   static constexpr int CPR = BK / 8;                          // 16-byte chunks per [row][k] row
   static constexpr int RPP = 256 / RB;                        // [row][k] rows per 256-byte bank period
@@ -90,9 +96,9 @@ struct DiagGeom : G {
 };
 
 // The stage geometries of the kernels.
-using SymGeom = NsGeom<64, 2>;    // Gram (ns_sym.hip)
-using PolyGeom = NsGeom<64, 2>;   // polynomial (ns_sym.hip; four 32-k slots measured no faster)
-using UpdGeom = NsGeom<32, 4>;    // update (ns_update.hip)
+using SymGeom = NsGeom<64, 2, 32>;    // Gram (ns_sym.hip)
+using PolyGeom = NsGeom<64, 2, 32>;   // polynomial (ns_sym.hip)
+using UpdGeom = NsGeom<64, 2, 32>;   // update (ns_update.hip)
 
 // ---------------------------------------------------------------------------
 // Operand addressing of the direct loads, shared by the kernels and the
@@ -264,6 +270,7 @@ __device__ __forceinline__ void pipeline(const int KT, const int nl, char* lds, 
   // (i % PER + 1) * GAP - 1; before the last sub-step min(nl, (H-1) PER) of a
   // stage's loads have been issued.
   constexpr int PER = LOADS / H;
+  constexpr int NMMA = G::NMMA;
   constexpr int GAP = PER > 0 ? NMMA / PER : 1;
   static_assert(!SPREAD || (LOADS % H == 0 && NMMA % PER == 0), "loads must spread evenly over the MFMAs");
   const int early = min(nl, (H - 1) * PER);

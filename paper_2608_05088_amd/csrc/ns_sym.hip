@@ -23,14 +23,15 @@ namespace {
 // Epilogue staging.  A diagonal tile stages the whole bf16 tile in LDS and
 // writes it out in 512-byte rows: written column-wise (each lane: four
 // consecutive rows of one column, 8 bytes into one staged row), rows padded by
-// 8 bytes so the 32 staged rows of one write land in distinct banks; written
-// row-wise (each lane: four consecutive columns), rows padded by 64 bytes.
-// Off-diagonal tiles go through per-wave regions: the sub-tile transposed (TN
-// rows of TM bf16, padded by 8 bytes), then as is (TM rows of TN bf16,
-// unpadded, halves swapped on alternate row pairs).
-constexpr int ST_PITCH_T = NS_TILE * 2 + 8;
+// 16 bytes so the 16 staged rows and two row groups of a half-wave's write
+// land in distinct banks; written row-wise (each lane: four consecutive
+// columns), rows padded by 64 bytes.  Off-diagonal tiles go through per-wave
+// regions: the sub-tile transposed (TN rows of TM bf16, padded by 16 bytes),
+// then as is (TM rows of TN bf16, unpadded, the 32-byte column units of a row
+// rotated by its row pair).
+constexpr int ST_PITCH_T = NS_TILE * 2 + 16;
 constexpr int ST_PITCH_R = NS_TILE * 2 + 64;
-constexpr int SYM_PITCH_T = TM * 2 + 8;
+constexpr int SYM_PITCH_T = TM * 2 + 16;
 constexpr int SYM_WAVE = TN * SYM_PITCH_T > TM * TN * 2 ? TN * SYM_PITCH_T : TM * TN * 2;
 constexpr int SYM_EPI_BYTES = NS_TILE * ST_PITCH_R;
 template <class G>
@@ -50,7 +51,8 @@ struct SymLds {
 template <class G, int PHASE>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
 void ns_gemm_sym_kernel(NsArgs args) {
-  constexpr int I = TM / 32, J = TN / 32;    // 32x32 blocks per wave
+  constexpr int I = TM / 16, J = TN / 16;    // 16x16 blocks per wave
+  static_assert(G::KSUB == 32, "v_mfma_f32_16x16x32_bf16 sub-steps");
 
   extern __shared__ __attribute__((aligned(16))) char lds[];
   // Every descriptor field the tile needs is read here, before any store, so
@@ -75,29 +77,34 @@ void ns_gemm_sym_kernel(NsArgs args) {
   const bool diag = t.ti == t.tj;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  // Sub-tile of each wave. On a diagonal tile only the 32 x 32 blocks on or
+  // Sub-tile of each wave. On a diagonal tile only the 16 x 16 blocks on or
   // above the block diagonal are computed (the others are their mirrors). The
   // two waves that share a SIMD (waves w and w + 4) then take sub-tiles with
-  // 8 + 0, 8 + 0, 7 + 3 and 3 + 7 such blocks, instead of the 3 + 0, 7 + 0,
-  // 8 + 3 and 8 + 7 of the plain order, so every matrix core gets a share.
+  // 32 + 0, 32 + 0, 26 + 10 and 10 + 26 such blocks, instead of the 10 + 0,
+  // 26 + 0, 32 + 10 and 32 + 26 of the plain order, so every matrix core gets
+  // a share.
   const int role = diag ? ((0x76540132u >> (4 * wave)) & 0xF) : wave;
   const int wr = role / (NW / 2), wc = role % (NW / 2);
 
-  f32x16 acc[I][J];
+  f32x4 acc[I][J];
 #pragma unroll
   for (int i = 0; i < I; ++i)
 #pragma unroll
     for (int j = 0; j < J; ++j)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+      for (int e = 0; e < 4; ++e) acc[i][j][e] = 0.f;
   const i32x4 rsP = buf_rsrc(P);
 
   // Diagonal and off-diagonal tiles run separate copies of the main loop, so
   // the block test exists only on diagonal tiles, and each has its own ring
   // geometry: G for off-diagonal tiles, DiagGeom<SymGeom> (64-k stages of the
   // row panel alone, four in the ring) for diagonal ones.
-  auto main_loop = [&](auto diag_tag) {
+  auto main_loop = [&](auto diag_tag, auto d_tag) {
     constexpr bool DIAG = decltype(diag_tag)::value;
+    // Diagonal tiles compute block (i, j) of the wave's sub-tile when
+    // i <= j + D, D = (wc TN - wr TM) / 16: a compile-time pattern per wave,
+    // so the skipped MFMAs cost no branch.
+    constexpr int D = decltype(d_tag)::value;
     using PG = std::conditional_t<DIAG, DiagGeom<SymGeom>, G>;
     using PL = SymLoads<std::conditional_t<DIAG, SymGeom, G>>;
     constexpr int H = PG::H, NL = PG::LOADS;
@@ -115,14 +122,16 @@ void ns_gemm_sym_kernel(NsArgs args) {
       voff[q] = (uint32_t)PL::voff(g, lane, row0, col0, ld);
       dst_off[q] = PL::dst(g);
     }
-    int offa[I][H], offb[J][H];
+    // MFMA operands: lane l holds k = 8 (l / 16) .. + 7 of row l % 16 of its
+    // block; a sub-step of 32 k spans chunks 4h .. 4h + 3.  The swizzle
+    // repeats every RPP * CPR rows, so block i sits 16 i rows below block 0.
+    static_assert(16 % (PG::RPP * PG::CPR) == 0, "16-row blocks keep the swizzle phase");
+    int offa[H], offb[H];
 #pragma unroll
     for (int h = 0; h < H; ++h) {
-      const int kc = 2 * h + (lane >> 5);
-#pragma unroll
-      for (int i = 0; i < I; ++i) offa[i][h] = PG::swz_rk(wr * TM + i * 32 + (lane & 31), kc);
-#pragma unroll
-      for (int j = 0; j < J; ++j) offb[j][h] = (DIAG ? 0 : PG::OPER_BYTES) + PG::swz_rk(wc * TN + j * 32 + (lane & 31), kc);
+      const int kc = 4 * h + (lane >> 4);
+      offa[h] = PG::swz_rk(wr * TM + (lane & 15), kc);
+      offb[h] = (DIAG ? 0 : PG::OPER_BYTES) + PG::swz_rk(wc * TN + (lane & 15), kc);
     }
     bf16x8 fa[2][I], fb[2][J];
     pipeline<PG, 1>(
@@ -133,9 +142,9 @@ void ns_gemm_sym_kernel(NsArgs args) {
         },
         [&](int buf, const char* st, int h) {
 #pragma unroll
-          for (int i = 0; i < I; ++i) fa[buf][i] = *reinterpret_cast<const bf16x8*>(st + offa[i][h]);
+          for (int i = 0; i < I; ++i) fa[buf][i] = *reinterpret_cast<const bf16x8*>(st + offa[h] + i * 16 * PG::RB);
 #pragma unroll
-          for (int j = 0; j < J; ++j) fb[buf][j] = *reinterpret_cast<const bf16x8*>(st + offb[j][h]);
+          for (int j = 0; j < J; ++j) fb[buf][j] = *reinterpret_cast<const bf16x8*>(st + offb[h] + j * 16 * PG::RB);
         },
         [&](int buf, auto&& after) {
 #pragma unroll
@@ -143,18 +152,26 @@ void ns_gemm_sym_kernel(NsArgs args) {
 #pragma unroll
             for (int j = 0; j < J; ++j) {
               // Diagonal tiles skip the blocks below the block diagonal.
-              if (!DIAG || (wr * TM) / 32 + i <= (wc * TN) / 32 + j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[buf][i], fb[buf][j], acc[i][j], 0, 0, 0);
+              if (!DIAG || i <= j + D)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[buf][i], fb[buf][j], acc[i][j], 0, 0, 0);
               after(i * J + j);
             }
         });
   };
-  if (diag) main_loop(std::true_type{});
-  else main_loop(std::false_type{});
+  if (!diag) {
+    main_loop(std::false_type{}, std::integral_constant<int, 0>{});
+  } else {
+    static_assert(TM == 2 * TN && TM / 16 == 8, "the four block patterns of a diagonal tile");
+    const int d = (wc * TN - wr * TM) / 16;   // -8, -4: none; 0, 4: a triangle; 8, 12: all
+    if (d < 0) main_loop(std::true_type{}, std::integral_constant<int, -8>{});
+    else if (d == 0) main_loop(std::true_type{}, std::integral_constant<int, 0>{});
+    else if (d == 4) main_loop(std::true_type{}, std::integral_constant<int, 4>{});
+    else main_loop(std::true_type{}, std::integral_constant<int, 8>{});
+  }
 
   // ---------------------------------------------------------------- epilogue
-  // acc[i][j][4g + e] = C(r, c): tile row r = wr*TM + i*32 + 8g + 4*(lane >> 5)
-  // + e, tile column c = wc*TN + j*32 + (lane & 31), so each lane holds four
+  // acc[i][j][e] = C(r, c): tile row r = wr*TM + i*16 + 4*(lane >> 4) + e,
+  // tile column c = wc*TN + j*16 + (lane & 15), so each lane holds four
   // consecutive rows of one column.  The final bf16 values are formed in
   // registers; the tile then leaves through LDS twice in whole rows: first
   // transposed (the mirror tile C^T), then as is after a 4 x 4 transpose
@@ -167,15 +184,15 @@ void ns_gemm_sym_kernel(NsArgs args) {
   const int lo_off = (poly && split) ? mp : 0;
   bf16_t* const out = poly ? Bm : Am;
   const int ldo = lo_off ? 2 * mp : mp;
-  const int rl0 = wr * TM + 4 * (lane >> 5);   // tile row of i = g = e = 0
-  const int cl0 = wc * TN + (lane & 31);       // tile column of j = 0
+  const int rl0 = wr * TM + 4 * (lane >> 4);   // tile row of i = e = 0
+  const int cl0 = wc * TN + (lane & 15);       // tile column of j = 0
 
   __syncthreads();   // every wave is done reading the operand ring
   if (poly) {
     // B' = a I + b A + c A A^T takes A(r, c) at each accumulator position.
     // A's tile goes to LDS as 256 rows in the [k][n] layout (direct loads),
     // and each lane reads its four rows of one column with one transposed
-    // read per (i, j, g).
+    // read per (i, j).
     const i32x4 rsA = buf_rsrc(Am);
 #pragma unroll
     for (int it = 0; it < NS_TILE * NS_TILE * 2 / (16 * NT); ++it) {
@@ -186,45 +203,45 @@ void ns_gemm_sym_kernel(NsArgs args) {
     wait_vm_c<0>();
     __syncthreads();
   }
-  uint2 hv[I][J][4];
+  uint2 hv[I][J];
   {
     const int r = (lane & 15) >> 2, q = lane & 3;
 #pragma unroll
     for (int i = 0; i < I; ++i)
 #pragma unroll
-      for (int j = 0; j < J; ++j)
+      for (int j = 0; j < J; ++j) {
+        float v[4];
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          float v[4];
+        for (int e = 0; e < 4; ++e) v[e] = acc[i][j][e];
+        if (poly) {
+          // In each 16-lane group (one row group, sixteen columns) lane
+          // q + 4r addresses row k0 + r, columns n0 + 4q .. n0 + 4q + 3.
+          const int k0 = rl0 + i * 16;
+          const int n0 = wc * TN + j * 16;
+          const i16x4 av = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(lds + swz_kn(k0 + r, n0 + 4 * q)));
+          const int R = row0 + k0, C = col0 + cl0 + j * 16;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * g + e];
-          if (poly) {
-            const int k0 = rl0 + i * 32 + 8 * g;
-            const int n0 = wc * TN + j * 32 + 16 * ((lane >> 4) & 1);
-            const i16x4 av = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(lds + swz_kn(k0 + r, n0 + 4 * q)));
-            const int R = row0 + k0, C = col0 + cl0 + j * 32;
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              v[e] = args.b * bf2f_((bf16_t)av[e]) + args.c * v[e] + (R + e == C ? args.a : 0.f);
-          }
-          hv[i][j][g].x = pack_bf16x2(sc * v[0], sc * v[1]);
-          hv[i][j][g].y = pack_bf16x2(sc * v[2], sc * v[3]);
-          if (lo_off) {
-            // Keep the low parts in acc (its values are no longer needed).
-            acc[i][j][4 * g + 0] = sc * v[0] - bf16_lo(hv[i][j][g].x);
-            acc[i][j][4 * g + 1] = sc * v[1] - bf16_hi(hv[i][j][g].x);
-            acc[i][j][4 * g + 2] = sc * v[2] - bf16_lo(hv[i][j][g].y);
-            acc[i][j][4 * g + 3] = sc * v[3] - bf16_hi(hv[i][j][g].y);
-          }
+          for (int e = 0; e < 4; ++e)
+            v[e] = args.b * bf2f_((bf16_t)av[e]) + args.c * v[e] + (R + e == C ? args.a : 0.f);
         }
+        hv[i][j].x = pack_bf16x2(sc * v[0], sc * v[1]);
+        hv[i][j].y = pack_bf16x2(sc * v[2], sc * v[3]);
+        if (lo_off) {
+          // Keep the low parts in acc (its values are no longer needed).
+          acc[i][j][0] = sc * v[0] - bf16_lo(hv[i][j].x);
+          acc[i][j][1] = sc * v[1] - bf16_hi(hv[i][j].x);
+          acc[i][j][2] = sc * v[2] - bf16_lo(hv[i][j].y);
+          acc[i][j][3] = sc * v[3] - bf16_hi(hv[i][j].y);
+        }
+      }
   }
 
   // Row-wise copy of accumulator group (i, j, g): a 4 x 4 transpose of
   // 16-bit values inside each lane quad, after which lane p of the quad holds
   // row p of the quad's four rows, its four columns.
   const int p = lane & 3;
-  auto quad_rows = [&](int i, int j, int g) {
-    const uint32_t A0 = hv[i][j][g].x, B0 = hv[i][j][g].y;   // rows (0,1), (2,3) of column p
+  auto quad_rows = [&](int i, int j) {
+    const uint32_t A0 = hv[i][j].x, B0 = hv[i][j].y;   // rows (0,1), (2,3) of column p
     const uint32_t A1 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)A0, 0xB1, 0xF, 0xF, true);   // lane p ^ 1
     const uint32_t B1 = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)B0, 0xB1, 0xF, 0xF, true);
     // Even lanes: row 0 (A) / row 2 (B) at columns p, p+1; odd lanes:
@@ -253,10 +270,8 @@ void ns_gemm_sym_kernel(NsArgs args) {
         for (int i = 0; i < I; ++i)
 #pragma unroll
           for (int j = 0; j < J; ++j)
-#pragma unroll
-            for (int g = 0; g < 4; ++g)
-              *reinterpret_cast<uint2*>(wreg + ((lane & 31) + j * 32) * SYM_PITCH_T +
-                                        (4 * (lane >> 5) + i * 32 + 8 * g) * 2) = hv[i][j][g];
+            *reinterpret_cast<uint2*>(wreg + ((lane & 15) + j * 16) * SYM_PITCH_T + (4 * (lane >> 4) + i * 16) * 2) =
+                hv[i][j];
         // Mirror: staged row x (of TM bf16) goes to row col0 + wc*TN + x.
         constexpr int TCH = TM * 2 / 16;
 #pragma unroll
@@ -270,27 +285,24 @@ void ns_gemm_sym_kernel(NsArgs args) {
           __builtin_nontemporal_store(v, reinterpret_cast<MALT_GLOBAL u32x4*>(
                                              gptr(out) + (size_t)(col0 + wc * TN + r) * ldo + off + row0 + wr * TM + ch * 8));
         }
-        // As is: 128-byte rows; rows 2 and 3 (mod 4) hold their two 64-byte
-        // halves swapped, so the four rows of one quad write land in four
-        // distinct 16-bank groups.
+        // As is: 128-byte rows of four 32-byte column units (j); unit j of
+        // row r sits at j ^ ((r >> 1) & 3), so the eight rows and four quads
+        // of a half-wave's write land in distinct banks.
 #pragma unroll
         for (int i = 0; i < I; ++i)
 #pragma unroll
-          for (int j = 0; j < J; ++j)
-#pragma unroll
-            for (int g = 0; g < 4; ++g) {
-              const int r = 4 * (lane >> 5) + i * 32 + 8 * g + p;
-              const int hf = j ^ ((r >> 1) & 1);
-              *reinterpret_cast<uint2*>(wreg + r * (TN * 2) + hf * 64 + (((lane & 31) >> 2) << 3)) =
-                  quad_rows(i, j, g);
-            }
+          for (int j = 0; j < J; ++j) {
+            const int r = 4 * (lane >> 4) + i * 16 + p;
+            const int u = j ^ ((r >> 1) & 3);
+            *reinterpret_cast<uint2*>(wreg + r * (TN * 2) + u * 32 + (((lane & 15) >> 2) << 3)) = quad_rows(i, j);
+          }
         constexpr int DCH = TN * 2 / 16;
 #pragma unroll
         for (int it = 0; it < TM * DCH / 64; ++it) {
           const int q = lane + 64 * it;
           const int r = q / DCH, ch = q % DCH;
-          const int hf = (ch >> 2) ^ ((r >> 1) & 1);
-          const u32x4 v = *reinterpret_cast<const u32x4*>(wreg + r * (TN * 2) + hf * 64 + (ch & 3) * 16);
+          const int u = (ch >> 1) ^ ((r >> 1) & 3);
+          const u32x4 v = *reinterpret_cast<const u32x4*>(wreg + r * (TN * 2) + u * 32 + (ch & 1) * 16);
           __builtin_nontemporal_store(v, reinterpret_cast<MALT_GLOBAL u32x4*>(
                                              gptr(out) + (size_t)(row0 + wr * TM + r) * ldo + off + col0 + wc * TN + ch * 8));
         }
@@ -305,18 +317,14 @@ void ns_gemm_sym_kernel(NsArgs args) {
     for (int i = 0; i < I; ++i)
 #pragma unroll
       for (int j = 0; j < J; ++j) {
-        const int br = (wr * TM) / 32 + i, bc = (wc * TN) / 32 + j;   // wave-uniform block coordinates
+        const int br = (wr * TM) / 16 + i, bc = (wc * TN) / 16 + j;   // wave-uniform block coordinates
         if (!diag || br <= bc)
-#pragma unroll
-          for (int g = 0; g < 4; ++g)
-            *reinterpret_cast<uint2*>(lds + (cl0 + j * 32) * ST_PITCH_T + (rl0 + i * 32 + 8 * g) * 2) = hv[i][j][g];
-        if (diag && br < bc)
-#pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const int rr = rl0 + i * 32 + 8 * g + p;
-            const int cc = wc * TN + j * 32 + ((lane & 31) & ~3);
-            *reinterpret_cast<uint2*>(lds + rr * ST_PITCH_T + cc * 2) = quad_rows(i, j, g);
-          }
+          *reinterpret_cast<uint2*>(lds + (cl0 + j * 16) * ST_PITCH_T + (rl0 + i * 16) * 2) = hv[i][j];
+        if (diag && br < bc) {
+          const int rr = rl0 + i * 16 + p;
+          const int cc = wc * TN + j * 16 + ((lane & 15) & ~3);
+          *reinterpret_cast<uint2*>(lds + rr * ST_PITCH_T + cc * 2) = quad_rows(i, j);
+        }
       }
     __syncthreads();
     // Staged row x goes to row col0 + x (the mirror tile; on a diagonal tile,
@@ -336,13 +344,11 @@ void ns_gemm_sym_kernel(NsArgs args) {
 #pragma unroll
     for (int i = 0; i < I; ++i)
 #pragma unroll
-      for (int j = 0; j < J; ++j)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int rr = rl0 + i * 32 + 8 * g + p;
-          const int cc = wc * TN + j * 32 + ((lane & 31) & ~3);
-          *reinterpret_cast<uint2*>(lds + rr * ST_PITCH_R + cc * 2) = quad_rows(i, j, g);
-        }
+      for (int j = 0; j < J; ++j) {
+        const int rr = rl0 + i * 16 + p;
+        const int cc = wc * TN + j * 16 + ((lane & 15) & ~3);
+        *reinterpret_cast<uint2*>(lds + rr * ST_PITCH_R + cc * 2) = quad_rows(i, j);
+      }
     __syncthreads();
 #pragma unroll 4
     for (int c = tid; c < CHUNKS; c += NT) {
@@ -357,12 +363,10 @@ void ns_gemm_sym_kernel(NsArgs args) {
 #pragma unroll
     for (int i = 0; i < I; ++i)
 #pragma unroll
-      for (int j = 0; j < J; ++j)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          hv[i][j][g].x = pack_bf16x2(acc[i][j][4 * g + 0], acc[i][j][4 * g + 1]);
-          hv[i][j][g].y = pack_bf16x2(acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
-        }
+      for (int j = 0; j < J; ++j) {
+        hv[i][j].x = pack_bf16x2(acc[i][j][0], acc[i][j][1]);
+        hv[i][j].y = pack_bf16x2(acc[i][j][2], acc[i][j][3]);
+      }
     emit(lo_off);
   }
 }

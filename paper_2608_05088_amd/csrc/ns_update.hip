@@ -4,9 +4,8 @@
 // consecutive output columns of one row.  X is read as a row-major [k][n]
 // stage tile through transposed LDS reads.  The last iteration also writes
 // the per-tile sums of O^2 and (L O R)^2 for the grafting norms.
-// Stages of 32 k in a four-slot ring, each stage's direct loads spread between
-// the MFMAs of the stage two ahead of it: the update contracts over K = m'
-// only, and on the GPT-2 Large set this ring beats two 64-k slots by 2.4%.
+// v_mfma_f32_16x16x32_bf16 on 16 x 16 blocks, in stages of 64 k (two 32-k
+// sub-steps) in a two-slot ring.
 #include "ns_common.h"
 
 namespace malt {
@@ -38,8 +37,8 @@ static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
 // ===========================================================================
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
 void ns_update_kernel(NsArgs args) {
-  constexpr int NB = TM / 32;                // B' fragments (output rows, MFMA B operand)
-  constexpr int NA = TN / 32;                // X fragments (output cols, MFMA A operand)
+  constexpr int NB = TM / 16;                // B' fragments (output rows, MFMA B operand)
+  constexpr int NA = TN / 16;                // X fragments (output cols, MFMA A operand)
 
   extern __shared__ __attribute__((aligned(16))) char lds[];
   // Every descriptor field the tile needs is read here, before any store, so
@@ -81,15 +80,18 @@ void ns_update_kernel(NsArgs args) {
     voff[q] = (uint32_t)(q < LOADS / 2 ? L::voff_b(g, lane, row0, ldb) : L::voff_x(g, lane, col0, np));
     dst_off[q] = L::dst(g);
   }
-  // B' fragments: rows of the output, k contiguous.
-  int offb[NB][H];
+  // MFMA operands (16 x 32 and 32 x 16): lane l holds k = 8 (l / 16) .. + 7
+  // of row / column l % 16 of its block.
+  // B' fragments: rows of the output, k contiguous.  The swizzle repeats
+  // every RPP * CPR rows, so block b sits 16 b rows below block 0.
+  static_assert(16 % (RPP * CPR) == 0, "16-row blocks keep the swizzle phase");
+  int offb[H];
 #pragma unroll
-  for (int h = 0; h < H; ++h)
-#pragma unroll
-    for (int b = 0; b < NB; ++b) offb[b][h] = swz_rk(wr * TM + b * 32 + (lane & 31), 2 * h + (lane >> 5));
+  for (int h = 0; h < H; ++h) offb[h] = swz_rk(wr * TM + (lane & 15), 4 * h + (lane >> 4));
   // X fragments through transposed reads: in each 16-lane group, lane
   // j = q + 4r addresses row k0 + r, columns n0 + 4q .. n0 + 4q + 3; the
-  // read hands lane i the four rows of column n0 + i.
+  // read hands lane i the four rows of column n0 + i.  Group l / 16 reads k
+  // rows 8 (l / 16) .. + 7 in two such reads.
   int offx[NA][2];
   {
     const int r = (lane & 15) >> 2, q = lane & 3;
@@ -97,22 +99,22 @@ void ns_update_kernel(NsArgs args) {
     for (int a = 0; a < NA; ++a)
 #pragma unroll
       for (int r2 = 0; r2 < 2; ++r2) {
-        const int k = 8 * (lane >> 5) + 4 * r2 + r;
-        const int n = wc * TN + a * 32 + 16 * ((lane >> 4) & 1) + 4 * q;
+        const int k = 8 * (lane >> 4) + 4 * r2 + r;
+        const int n = wc * TN + a * 16 + 4 * q;
         offx[a][r2] = OPER_BYTES + swz_kn(k, n);
       }
   }
 
-  f32x16 acc[NA][NB];
+  f32x4 acc[NA][NB];
 #pragma unroll
   for (int a = 0; a < NA; ++a)
 #pragma unroll
     for (int b = 0; b < NB; ++b)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.f;
+      for (int e = 0; e < 4; ++e) acc[a][b][e] = 0.f;
   bf16x8 fx[2][NA], fb[2][NB];
 
-  pipeline<G, 2>(
+  pipeline<G, 1>(
       K / BK, LOADS, lds,
       [&](int kt, int q) {   // q < LOADS / 2: B' rows, else X k-rows
         const uint32_t la = lds_u32(lds + (kt % STAGES) * STAGE_BYTES + dst_off[q]);
@@ -121,13 +123,13 @@ void ns_update_kernel(NsArgs args) {
       },
       [&](int buf, const char* st, int h) {
 #pragma unroll
-        for (int b = 0; b < NB; ++b) fb[buf][b] = *reinterpret_cast<const bf16x8*>(st + offb[b][h]);
+        for (int b = 0; b < NB; ++b) fb[buf][b] = *reinterpret_cast<const bf16x8*>(st + offb[h] + b * 16 * RB);
 #pragma unroll
         for (int a = 0; a < NA; ++a) {
           const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_i16x4_t*)(st + offx[a][0] + h * 16 * KN_ROW));
+              (lds_i16x4_t*)(st + offx[a][0] + h * 32 * KN_ROW));
           const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_i16x4_t*)(st + offx[a][1] + h * 16 * KN_ROW));
+              (lds_i16x4_t*)(st + offx[a][1] + h * 32 * KN_ROW));
           fx[buf][a] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
         }
       },
@@ -136,21 +138,21 @@ void ns_update_kernel(NsArgs args) {
         for (int a = 0; a < NA; ++a)
 #pragma unroll
           for (int b = 0; b < NB; ++b) {
-            acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fx[buf][a], fb[buf][b], acc[a][b], 0, 0, 0);
+            acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fx[buf][a], fb[buf][b], acc[a][b], 0, 0, 0);
             after(a * NB + b);
           }
       });
 
   // ---------------------------------------------------------------- epilogue
-  // acc[a][b][4g + e] = C(m, n + e), m = row0 + wr*TM + b*32 + (lane & 31),
-  // n = col0 + wc*TN + a*32 + 8g + 4*(lane >> 5): four consecutive bf16 per
-  // lane.  Each wave copies its own TM x TN sub-tile to a private LDS region
-  // and writes it out in whole 128-byte row pieces, not as 16-byte pieces of
-  // 32 rows.  A wave reads back only what it staged, so no barrier separates
+  // acc[a][b][e] = C(m, n + e), m = row0 + wr*TM + b*16 + (lane & 15),
+  // n = col0 + wc*TN + a*16 + 4*(lane >> 4): four consecutive bf16 per lane.
+  // Each wave copies its own TM x TN sub-tile to a private LDS region and
+  // writes it out in whole 128-byte row pieces, not as 8-byte pieces of 16
+  // rows.  A wave reads back only what it staged, so no barrier separates
   // the two and each wave leaves the epilogue at its own pace.
-  const int ml0 = wr * TM + (lane & 31);          // tile-local row of b = 0
-  const int nl0 = wc * TN + 4 * (lane >> 5);      // tile-local column of a = g = 0
-  const int sr0 = lane & 31, sc0 = 4 * (lane >> 5);   // the same within the sub-tile
+  const int ml0 = wr * TM + (lane & 15);          // tile-local row of b = 0
+  const int nl0 = wc * TN + 4 * (lane >> 4);      // tile-local column of a = 0
+  const int sr0 = lane & 15, sc0 = 4 * (lane >> 4);   // the same within the sub-tile
   char* const sto = lds + wave * UPD_WAVE;
   __syncthreads();   // every wave is done reading the operand ring
   float o2 = 0.f, d2 = 0.f;
@@ -158,34 +160,31 @@ void ns_update_kernel(NsArgs args) {
 #pragma unroll
     for (int b = 0; b < NB; ++b)
 #pragma unroll
-      for (int a = 0; a < NA; ++a)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          uint2 pk;
-          pk.x = pack_bf16x2(sc * acc[a][b][4 * g + 0], sc * acc[a][b][4 * g + 1]);
-          pk.y = pack_bf16x2(sc * acc[a][b][4 * g + 2], sc * acc[a][b][4 * g + 3]);
-          *reinterpret_cast<uint2*>(sto + (sr0 + b * 32) * UPD_PITCH + (sc0 + a * 32 + 8 * g) * 2) = pk;
-        }
+      for (int a = 0; a < NA; ++a) {
+        uint2 pk;
+        pk.x = pack_bf16x2(sc * acc[a][b][0], sc * acc[a][b][1]);
+        pk.y = pack_bf16x2(sc * acc[a][b][2], sc * acc[a][b][3]);
+        *reinterpret_cast<uint2*>(sto + (sr0 + b * 16) * UPD_PITCH + (sc0 + a * 16) * 2) = pk;
+      }
   } else {
     // Last iteration: also the per-tile sums of O^2 and (L O R)^2, from the
     // rounded O.  Canonical (m, n) is W(m, n) for wide and W(n, m) for tall
     // matrices.
     const float* const Lm = tall ? Rv : Lv;   // factor indexed by the canonical row
     const float* const Ln = tall ? Lv : Rv;   // factor indexed by the canonical column
-    // (Lm O Ln)^2 = Lm^2 Ln^2 O^2: four squared row factors per lane, four
-    // squared column factors per (a, g).
+    // (Lm O Ln)^2 = Lm^2 Ln^2 O^2: NB squared row factors per lane, four
+    // squared column factors per a.
     float lm2[NB];
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
-      const int m = row0 + ml0 + b * 32;
+      const int m = row0 + ml0 + b * 16;
       const float l = m < mc ? Lm[m] : 0.f;
       lm2[b] = l * l;
     }
 #pragma unroll
     for (int a = 0; a < NA; ++a) {
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int nl = nl0 + a * 32 + 8 * g;
+      {
+        const int nl = nl0 + a * 16;
         const int n = col0 + nl;
         float ln2[4];
 #pragma unroll
@@ -195,11 +194,11 @@ void ns_update_kernel(NsArgs args) {
         }
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
-          const int m = row0 + ml0 + b * 32;
+          const int m = row0 + ml0 + b * 16;
           uint2 pk;
-          pk.x = pack_bf16x2(sc * acc[a][b][4 * g + 0], sc * acc[a][b][4 * g + 1]);
-          pk.y = pack_bf16x2(sc * acc[a][b][4 * g + 2], sc * acc[a][b][4 * g + 3]);
-          *reinterpret_cast<uint2*>(sto + (sr0 + b * 32) * UPD_PITCH + (sc0 + a * 32 + 8 * g) * 2) = pk;
+          pk.x = pack_bf16x2(sc * acc[a][b][0], sc * acc[a][b][1]);
+          pk.y = pack_bf16x2(sc * acc[a][b][2], sc * acc[a][b][3]);
+          *reinterpret_cast<uint2*>(sto + (sr0 + b * 16) * UPD_PITCH + (sc0 + a * 16) * 2) = pk;
           const float ov[4] = {bf16_lo(pk.x), bf16_hi(pk.x), bf16_lo(pk.y), bf16_hi(pk.y)};
           float rowo = 0.f, rowd = 0.f;
 #pragma unroll
@@ -213,7 +212,7 @@ void ns_update_kernel(NsArgs args) {
             d2 += lm2[b] * rowd;
           }
         }
-        asm volatile("" ::: "memory");   // keep the column-factor loads of one (a, g) at a time
+        asm volatile("" ::: "memory");   // keep the column-factor loads of one a at a time
       }
     }
   }
