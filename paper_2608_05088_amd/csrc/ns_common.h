@@ -75,10 +75,19 @@ struct NsGeom {
 };
 
 // [k][n] tile: rows of 256 bf16 (512 bytes), 16-byte chunk c stored at
-// c ^ (4 * (k & 3)): the 16 lanes of one transposed read (four rows x 32
-// contiguous bytes) hit 16 distinct 4-bank groups.
+// swz_chunk<GB>(k, c) = c ^ 4 (k & 3) ^ 2 (bit GB of k): the 16 lanes of one
+// transposed read (four rows x 32 contiguous bytes) hit 16 distinct 4-bank
+// groups, and the second 16-lane group of a half-wave, whose rows differ from
+// the first's in bit GB and whose columns are the same, hits the other 16.
+// GB = 3 for the update's X stages (the two groups read k-rows 8 apart), 2
+// for the polynomial's A tile (4 apart).
+template <int GB>
+__host__ __device__ constexpr int swz_chunk(int k, int c) {
+  return c ^ (4 * (k & 3)) ^ (2 * ((k >> GB) & 1));
+}
+template <int GB>
 __host__ __device__ constexpr int swz_kn(int k, int n) {
-  return k * KN_ROW + (((n >> 3) ^ (4 * (k & 3))) << 4) + ((n & 7) << 1);
+  return k * KN_ROW + (swz_chunk<GB>(k, n >> 3) << 4) + ((n & 7) << 1);
 }
 
 // Diagonal tiles of the symmetric products load one operand panel per stage
@@ -133,7 +142,7 @@ struct SymLoads {
 // Polynomial epilogue: A's 256 x 256 output tile (row0, col0) loaded into LDS
 // in the [k][n] layout, 16-byte chunk c (0 <= c < 8192) from tile row c / 32.
 __host__ __device__ constexpr uint64_t poly_a_tile_off(int c, int row0, int col0, int mp) {
-  return ((uint64_t)(row0 + (c >> 5)) * (uint64_t)mp + col0 + (((c & 31) ^ (4 * ((c >> 5) & 3))) * 8)) * 2;
+  return ((uint64_t)(row0 + (c >> 5)) * (uint64_t)mp + col0 + (uint64_t)swz_chunk<2>(c >> 5, c & 31) * 8) * 2;
 }
 
 // Update: loads g < LOADS_P read rows row0 .. of B' (row pitch ldb, [row][k]),
@@ -152,7 +161,7 @@ struct UpdLoads {
   }
   __host__ __device__ static constexpr uint64_t voff_x(int g, int lane, int col0, int np) {
     return ((uint64_t)((g - LOADS_P) * KROWS_PER_LOAD + lane / 32) * (uint64_t)np + col0 +
-            (uint64_t)(((lane % 32) ^ (4 * (((g - LOADS_P) * KROWS_PER_LOAD + lane / 32) & 3))) * 8)) *
+            (uint64_t)swz_chunk<3>((g - LOADS_P) * KROWS_PER_LOAD + lane / 32, lane % 32) * 8) *
            2;
   }
   __host__ __device__ static constexpr uint64_t soff_b(int kt) { return (uint64_t)kt * G::BK * 2; }

@@ -218,7 +218,7 @@ void ns_gemm_sym_kernel(NsArgs args) {
           // q + 4r addresses row k0 + r, columns n0 + 4q .. n0 + 4q + 3.
           const int k0 = rl0 + i * 16;
           const int n0 = wc * TN + j * 16;
-          const i16x4 av = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(lds + swz_kn(k0 + r, n0 + 4 * q)));
+          const i16x4 av = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(lds + swz_kn<2>(k0 + r, n0 + 4 * q)));
           const int R = row0 + k0, C = col0 + cl0 + j * 16;
 #pragma unroll
           for (int e = 0; e < 4; ++e)

@@ -101,7 +101,7 @@ void ns_update_kernel(NsArgs args) {
       for (int r2 = 0; r2 < 2; ++r2) {
         const int k = 8 * (lane >> 4) + 4 * r2 + r;
         const int n = wc * TN + a * 16 + 4 * q;
-        offx[a][r2] = OPER_BYTES + swz_kn(k, n);
+        offx[a][r2] = OPER_BYTES + swz_kn<3>(k, n);
       }
   }
 
