@@ -5,12 +5,13 @@
 // each instantiate the pipeline with their own stage geometry (NsGeom).
 //
 // Every kernel: one 256 x 256 output tile per workgroup of 8 waves (2 per
-// SIMD), each wave owning a 128 x 64 sub-tile as 32x32 blocks of
-// v_mfma_f32_32x32x16_bf16.  Operand stages of BK k-values stream from global
-// memory straight into an LDS ring (buffer_load ... lds, 16 bytes per lane),
-// STAGES deep, one barrier per stage; fragments are double-buffered in
-// registers so the reads for the next 16-k sub-step are in flight while the
-// current one multiplies.
+// SIMD), each wave owning a 128 x 64 sub-tile as 16x16 blocks of
+// v_mfma_f32_16x16x32_bf16 (under the chip's power budget this shape sustains
+// a higher rate than 32x32x16 with random operands).  Operand stages of BK
+// k-values stream from global memory straight into an LDS ring (buffer_load
+// ... lds, 16 bytes per lane), STAGES deep, one barrier per stage; fragments
+// are double-buffered in registers so the reads for the next 32-k sub-step
+// are in flight while the current one multiplies.
 //
 // NT operands (rows with k contiguous) use ds_read_b128 fragments from an
 // XOR-swizzled [row][k] tile.  A [k][n] operand (X in the update) is read with
