@@ -95,10 +95,11 @@ void ns_gemm_sym_kernel(NsArgs args) {
       for (int e = 0; e < 4; ++e) acc[i][j][e] = 0.f;
   const i32x4 rsP = buf_rsrc(P);
 
-  // Diagonal and off-diagonal tiles run separate copies of the main loop, so
-  // the block test exists only on diagonal tiles, and each has its own ring
-  // geometry: G for off-diagonal tiles, DiagGeom<SymGeom> (64-k stages of the
-  // row panel alone, four in the ring) for diagonal ones.
+  // Off-diagonal tiles and the four block patterns of diagonal tiles run
+  // separate copies of the main loop, so no copy tests blocks at run time, and
+  // each tile kind has its own ring geometry: G for off-diagonal tiles,
+  // DiagGeom<SymGeom> (64-k stages of the row panel alone, four in the ring)
+  // for diagonal ones.
   auto main_loop = [&](auto diag_tag, auto d_tag) {
     constexpr bool DIAG = decltype(diag_tag)::value;
     // Diagonal tiles compute block (i, j) of the wave's sub-tile when
@@ -162,7 +163,9 @@ void ns_gemm_sym_kernel(NsArgs args) {
     main_loop(std::false_type{}, std::integral_constant<int, 0>{});
   } else {
     static_assert(TM == 2 * TN && TM / 16 == 8, "the four block patterns of a diagonal tile");
-    const int d = (wc * TN - wr * TM) / 16;   // -8, -4: none; 0, 4: a triangle; 8, 12: all
+    // d = -8, -4: no block; 0: the upper triangle; 4: all but the 6 blocks of
+    // the lower-left corner; 8, 12: every block.
+    const int d = (wc * TN - wr * TM) / 16;
     if (d < 0) main_loop(std::true_type{}, std::integral_constant<int, -8>{});
     else if (d == 0) main_loop(std::true_type{}, std::integral_constant<int, 0>{});
     else if (d == 4) main_loop(std::true_type{}, std::integral_constant<int, 4>{});
