@@ -247,6 +247,9 @@ __device__ __forceinline__ uint32_t lds_u32(const void* p) {
 //   read(buf, st, h)  fragment reads of sub-step h of the stage at st into buf
 //   mma(buf, after)   the MFMAs of the fragments in buf, calling after(j) once
 //                     the j-th of the NMMA has been issued
+//   pre(kt, h, st)    extra work of the kernel at the start of sub-step h of
+//                     stage kt (slot st), before the next sub-step's fragment
+//                     reads: the registers of those fragments are free here
 // nl is the number of loads this wave issues per stage (LOADS, or fewer); RPM
 // the LDS fragment reads placed after each MFMA.
 //
@@ -258,9 +261,9 @@ __device__ __forceinline__ uint32_t lds_u32(const void* p) {
 // after an equal share of the MFMAs), into the slot stage kt - 1 freed.  The
 // loads of STAGES - 2 stages stay in flight across every barrier, and no wave
 // issues a burst of loads while its SIMD partner waits for the matrix core.
-template <class G, int RPM, class Issue, class Read, class Mma>
+template <class G, int RPM, class Issue, class Read, class Pre, class Mma>
 __device__ __forceinline__ void pipeline(const int KT, const int nl, char* lds, Issue&& issue, Read&& read,
-                                         Mma&& mma) {
+                                         Pre&& pre, Mma&& mma) {
   constexpr int STAGES = G::STAGES, H = G::H, LOADS = G::LOADS, STAGE_BYTES = G::STAGE_BYTES;
   constexpr bool SPREAD = G::SPREAD;
   constexpr int PRE = SPREAD ? STAGES - 1 : STAGES;   // stages loaded before the loop
@@ -292,6 +295,7 @@ __device__ __forceinline__ void pipeline(const int KT, const int nl, char* lds, 
 #pragma unroll
     for (int h = 0; h < H; ++h) {
       const int c = h & 1;
+      pre(kt, h, st);
       if (h + 1 < H) {
         read(c ^ 1, st, h + 1);
       } else if (steady || kt + 1 < KT) {
@@ -343,6 +347,12 @@ __device__ __forceinline__ void pipeline(const int KT, const int nl, char* lds, 
   int kt = 0;
   for (; kt < KT - LEAD; ++kt) body(kt, std::true_type{});
   for (; kt < KT; ++kt) body(kt, std::false_type{});
+}
+
+template <class G, int RPM, class Issue, class Read, class Mma>
+__device__ __forceinline__ void pipeline(const int KT, const int nl, char* lds, Issue&& issue, Read&& read,
+                                         Mma&& mma) {
+  pipeline<G, RPM>(KT, nl, lds, issue, read, [](int, int, const char*) {}, mma);
 }
 
 }  // namespace ns

@@ -76,6 +76,12 @@ void ns_gemm_sym_kernel(NsArgs args) {
   // the row panel only and reads both operands from it.
   const bool diag = t.ti == t.tj;
 
+  // Polynomial with c != 0: B' = c (A A^T + (b/c) A) + a I, the (b/c) A term
+  // added to the accumulators inside the main loop (below).  With c = 0 the
+  // epilogue reloads A's tile instead.
+  const bool fuse = phase == PH_POLY && args.c != 0.f;
+  const float beta = fuse ? args.b / args.c : 0.f;
+
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   // Sub-tile of each wave. On a diagonal tile only the 16 x 16 blocks on or
   // above the block diagonal are computed (the others are their mirrors). The
@@ -134,6 +140,46 @@ void ns_gemm_sym_kernel(NsArgs args) {
       offa[h] = PG::swz_rk(wr * TM + (lane & 15), kc);
       offb[h] = (DIAG ? 0 : PG::OPER_BYTES) + PG::swz_rk(wc * TN + (lane & 15), kc);
     }
+    // The (b/c) A term of the polynomial.  A is symmetric, so the entry
+    // A(r, c) of accumulator position (r, c) is k = r of the tile-column
+    // panel's row c: the stage holding k = row0 + wr TM .. + 63 has block rows
+    // 0..3 of the wave's sub-tile, the next stage block rows 4..7, and each
+    // lane's four consecutive rows of one column are 8 contiguous bytes.  The
+    // first stage is read in its first sub-step and the second in its second,
+    // each before the next sub-step's fragment reads, whose registers are
+    // still free there.
+    static_assert(PG::BK == 64 && 4 * 16 == PG::BK, "four block rows per stage");
+    const int kta = fuse ? (row0 + wr * TM) / PG::BK : -2;
+    auto add_a = [&](auto s_tag, const char* st) {
+      constexpr int S = decltype(s_tag)::value;
+      // Offsets formed here from a copy of the lane id the compiler cannot
+      // hoist: the main loop has no registers to keep them in.
+      int l = lane;
+      asm volatile("" : "+v"(l));
+      // Two block rows at a time (16 registers of values).
+#pragma unroll
+      for (int i0 = 0; i0 < 4; i0 += 2) {
+        uint2 w[2][J];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          const int ao = (DIAG ? 0 : PG::OPER_BYTES) + wc * TN * PG::RB +
+                         PG::swz_rk(l & 15, 2 * (i0 + i) + (l >> 5)) + ((l >> 4) & 1) * 8;
+#pragma unroll
+          for (int j = 0; j < J; ++j) w[i][j] = *reinterpret_cast<const uint2*>(st + ao + j * 16 * PG::RB);
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < J; ++j)
+            if (!DIAG || 4 * S + i0 + i <= j + D) {
+              f32x4& a = acc[4 * S + i0 + i][j];
+              a[0] = fmaf(beta, __uint_as_float(w[i][j].x << 16), a[0]);
+              a[1] = fmaf(beta, __uint_as_float(w[i][j].x & 0xffff0000u), a[1]);
+              a[2] = fmaf(beta, __uint_as_float(w[i][j].y << 16), a[2]);
+              a[3] = fmaf(beta, __uint_as_float(w[i][j].y & 0xffff0000u), a[3]);
+            }
+      }
+    };
     bf16x8 fa[2][I], fb[2][J];
     pipeline<PG, 1>(
         K / PG::BK, NL, lds,
@@ -146,6 +192,14 @@ void ns_gemm_sym_kernel(NsArgs args) {
           for (int i = 0; i < I; ++i) fa[buf][i] = *reinterpret_cast<const bf16x8*>(st + offa[h] + i * 16 * PG::RB);
 #pragma unroll
           for (int j = 0; j < J; ++j) fb[buf][j] = *reinterpret_cast<const bf16x8*>(st + offb[h] + j * 16 * PG::RB);
+        },
+        [&](int kt, int h, const char* st) {
+          if constexpr (PHASE == PH_POLY && !(DIAG && D < 0)) {
+            // One test per sub-step: nested tests of the stage would make
+            // the compiler copy the accumulators between branches.
+            if (h == 0 && kt == kta) add_a(std::integral_constant<int, 0>{}, st);
+            if (h == 1 && kt == kta + 1) add_a(std::integral_constant<int, 1>{}, st);
+          }
         },
         [&](int buf, auto&& after) {
 #pragma unroll
@@ -191,11 +245,11 @@ void ns_gemm_sym_kernel(NsArgs args) {
   const int cl0 = wc * TN + (lane & 15);       // tile column of j = 0
 
   __syncthreads();   // every wave is done reading the operand ring
-  if (poly) {
-    // B' = a I + b A + c A A^T takes A(r, c) at each accumulator position.
-    // A's tile goes to LDS as 256 rows in the [k][n] layout (direct loads),
-    // and each lane reads its four rows of one column with one transposed
-    // read per (i, j).
+  if (poly && !fuse) {
+    // c = 0: B' = a I + b A + c A A^T takes A(r, c) at each accumulator
+    // position. A's tile goes to LDS as 256 rows in the [k][n] layout (direct
+    // loads), and each lane reads its four rows of one column with one
+    // transposed read per (i, j).
     const i32x4 rsA = buf_rsrc(Am);
 #pragma unroll
     for (int it = 0; it < NS_TILE * NS_TILE * 2 / (16 * NT); ++it) {
@@ -217,15 +271,21 @@ void ns_gemm_sym_kernel(NsArgs args) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) v[e] = acc[i][j][e];
         if (poly) {
-          // In each 16-lane group (one row group, sixteen columns) lane
-          // q + 4r addresses row k0 + r, columns n0 + 4q .. n0 + 4q + 3.
           const int k0 = rl0 + i * 16;
-          const int n0 = wc * TN + j * 16;
-          const i16x4 av = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(lds + swz_kn<2>(k0 + r, n0 + 4 * q)));
           const int R = row0 + k0, C = col0 + cl0 + j * 16;
+          if (fuse) {
 #pragma unroll
-          for (int e = 0; e < 4; ++e)
-            v[e] = args.b * bf2f_((bf16_t)av[e]) + args.c * v[e] + (R + e == C ? args.a : 0.f);
+            for (int e = 0; e < 4; ++e) v[e] = args.c * v[e] + (R + e == C ? args.a : 0.f);
+          } else {
+            // In each 16-lane group (one row group, sixteen columns) lane
+            // q + 4r addresses row k0 + r, columns n0 + 4q .. n0 + 4q + 3.
+            const int n0 = wc * TN + j * 16;
+            const i16x4 av =
+                __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(lds + swz_kn<2>(k0 + r, n0 + 4 * q)));
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              v[e] = args.b * bf2f_((bf16_t)av[e]) + args.c * v[e] + (R + e == C ? args.a : 0.f);
+          }
         }
         hv[i][j].x = pack_bf16x2(sc * v[0], sc * v[1]);
         hv[i][j].y = pack_bf16x2(sc * v[2], sc * v[3]);
