@@ -249,6 +249,69 @@ def test_gram_and_polynomial_outputs_are_exactly_symmetric(variant):
         assert float(dv["A"][mc:, :].abs().max().item() if dv["A"].shape[0] > mc else 0.0) == 0.0
 
 
+def _bf16_ulp(v):
+    """Spacing of bf16 numbers at |v| (8 significant bits)."""
+    a = np.maximum(np.abs(v), np.finfo(np.float32).tiny)
+    return np.exp2(np.floor(np.log2(a)) - 7)
+
+
+def _check_rounded_product(got, ref, bound, label, split_lo=None):
+    """got (bf16 values, or a hi/lo pair) against the fp64 ref: within one bf16
+    spacing of ref plus the fp32 accumulation bound, and mostly the exact
+    round-to-nearest of ref."""
+    if split_lo is None:
+        err = np.abs(got - ref)
+        assert np.all(err <= _bf16_ulp(ref) + bound), f"{label}: max excess {np.max(err - _bf16_ulp(ref) - bound):.3e}"
+        rne = (_bf16_rne(ref.astype(np.float32)).astype(np.uint32) << 16).view(np.float32)
+        exact = float(np.mean(got == rne))
+        assert exact > 0.98, f"{label}: only {exact:.4f} of the entries are the rounded product"
+    else:
+        err = np.abs(got + split_lo - ref)
+        assert np.all(err <= 2.0 ** -15 * np.abs(ref) + bound + 1e-30), f"{label}: hi + lo off by {err.max():.3e}"
+
+
+@pytest.mark.parametrize("abc,ns_steps", [((3.4445, -4.7750, 2.0315), 1), ((3.4445, -4.7750, 2.0315), 2),
+                                          ((1.5, -0.5, 0.0), 1), ((2.0, -1.5, 0.5), 3)])
+def test_gram_and_polynomial_against_fp64_of_their_own_inputs(abc, ns_steps):
+    # Kernel-level check of the two symmetric products, on the GPU's own bf16
+    # operands: the last iteration's A and B' (debug views) against A = s X X^T
+    # (first iteration: X = X0, s = sigma^2) and B' = a I + b A + c A A computed
+    # in fp64 from the same bf16 values.  c != 0 adds b A inside the
+    # polynomial's main loop, c = 0 reloads A in its epilogue; the shapes cover
+    # diagonal and off-diagonal tiles, a tall matrix, a 1280-square matrix and a
+    # split one (m' <= 128: B' as a bf16 hi/lo pair).
+    import torch
+    a, b, c = abc
+    shapes = [(700, 1500), (1500, 300), (1280, 1280), (64, 5000)]
+    say(f"[parity] symmetric products vs fp64 of their inputs {abc} ns_steps={ns_steps} {shapes}")
+    W0 = [wl.weight(97, i, s) for i, s in enumerate(shapes)]
+    G = [wl.grad(97, 1, i, s, "row_loguniform") for i, s in enumerate(shapes)]
+    plan = lm.Plan(shapes, "malt")
+    Wd, Gd = to_dev(W0), to_dev(G)
+    plan.step(Wd, Gd, lm.make_hparams(lr=1e-2, ns_steps=ns_steps, ns_a=a, ns_b=b, ns_c=c))
+    torch.cuda.synchronize()
+    u = 2.0 ** -23
+    for i, (m, n) in enumerate(shapes):
+        dv = plan.debug_views(i)
+        A = dv["A"].float().cpu().numpy().astype(np.float64)
+        p = A.shape[0]
+        if ns_steps == 1:
+            X = dv["X0"].float().cpu().numpy().astype(np.float64)
+            X = X.T if m > n else X
+            Xp = np.zeros((p, X.shape[1]))
+            Xp[:X.shape[0]] = X
+            sig = np.float32(dv["scalars"]["sigma"].item())
+            s = float(np.float32(sig * sig))
+            ref = s * (Xp @ Xp.T)
+            bound = s * (np.abs(Xp) @ np.abs(Xp).T) * Xp.shape[1] * u + 2 * u * np.abs(ref)
+            _check_rounded_product(A, ref, bound, f"matrix {i} {m}x{n} A")
+        ref = a * np.eye(p) + b * A + c * (A @ A)
+        bound = (abs(c) * (np.abs(A) @ np.abs(A)) * p + abs(b) * np.abs(A) + abs(a)) * u * 4
+        B = dv["B"].float().cpu().numpy().astype(np.float64)
+        lo = dv["B_lo"].float().cpu().numpy().astype(np.float64) if "B_lo" in dv else None
+        _check_rounded_product(B, ref, bound, f"matrix {i} {m}x{n} B'", split_lo=lo)
+
+
 # Four shape kinds (a split contraction with K = 2 m', unsplit K = 768, a tall
 # matrix, a wide split one) repeated: 496 update tiles, more than one per
 # compute unit, of different K and pitch in one grouped launch.
