@@ -62,7 +62,9 @@ void ns_update_kernel(NsArgs args) {
   const float sc = args.first ? (float)d->scal[SC_SIGMA] : 1.f;
   const int row0 = t.ti * NS_TILE, col0 = t.tj * NS_TILE;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // wave is read as uniform, so each direct load's LDS address (m0) is scalar
+  // arithmetic, not a vector add and a readfirstlane per load.
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wr = wave / (NW / 2), wc = wave % (NW / 2);
 
   // Direct-load sources as 32-bit byte offsets into the B' and X buffers
