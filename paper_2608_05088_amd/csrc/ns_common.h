@@ -251,9 +251,10 @@ __device__ __forceinline__ uint32_t lds_u32(const void* p) {
 //                     stage kt (slot st), before the next sub-step's fragment
 //                     reads: the registers of those fragments are free here
 // nl is the number of loads this wave issues per stage (LOADS, or fewer); RPM
-// the LDS fragment reads placed after each MFMA.  LATE (burst only): a stage's
-// loads go out from among the MFMAs of the sub-step after the barrier instead
-// of before them, so the matrix cores restart first.
+// the LDS fragment reads placed after each MFMA.  LATE (burst only): the
+// first LATE of a stage's loads go out from among the MFMAs of the sub-step
+// after the barrier instead of before them, so the matrix cores restart
+// first; the rest go out right after the barrier.
 //
 // Burst (two slots): at the barrier closing stage kt, stage kt + 1 has landed
 // and every wave is done with slot kt % 2, which then receives all of stage
@@ -263,7 +264,7 @@ __device__ __forceinline__ uint32_t lds_u32(const void* p) {
 // after an equal share of the MFMAs), into the slot stage kt - 1 freed.  The
 // loads of STAGES - 2 stages stay in flight across every barrier, and no wave
 // issues a burst of loads while its SIMD partner waits for the matrix core.
-template <class G, int RPM, bool LATE, class Issue, class Read, class Pre, class Mma>
+template <class G, int RPM, int LATE, class Issue, class Read, class Pre, class Mma>
 __device__ __forceinline__ void pipeline(const int KT, const int nl, char* lds, Issue&& issue, Read&& read,
                                          Pre&& pre, Mma&& mma) {
   constexpr int STAGES = G::STAGES, H = G::H, LOADS = G::LOADS, STAGE_BYTES = G::STAGE_BYTES;
@@ -318,9 +319,9 @@ __device__ __forceinline__ void pipeline(const int KT, const int nl, char* lds, 
         }
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");
-        if constexpr (!SPREAD && !LATE && steady) {
+        if constexpr (!SPREAD && steady) {
 #pragma unroll
-          for (int i = 0; i < LOADS; ++i)
+          for (int i = LATE; i < LOADS; ++i)
             if (i < nl) issue(kt + STAGES, i);
         }
         read(c ^ 1, lds + ((kt + 1) % STAGES) * STAGE_BYTES, 0);
@@ -332,10 +333,10 @@ __device__ __forceinline__ void pipeline(const int KT, const int nl, char* lds, 
             if (i < nl) issue(kt + STAGES - 1, i);
           }
         }
-        if constexpr (!SPREAD && LATE && steady) {
+        if constexpr (!SPREAD && LATE > 0 && steady) {
           // The compiler keeps the loads' order with the fragment reads (the
           // loads are asm with a memory clobber) but may move MFMAs ahead.
-          if (h == H - 1 && j < LOADS && j < nl) issue(kt + STAGES, j);
+          if (h == H - 1 && j < LATE && j < nl) issue(kt + STAGES, j);
         }
       });
       // Interleave the sub-step's MFMAs with the fragment reads for the next
@@ -359,7 +360,7 @@ __device__ __forceinline__ void pipeline(const int KT, const int nl, char* lds, 
 template <class G, int RPM, class Issue, class Read, class Mma>
 __device__ __forceinline__ void pipeline(const int KT, const int nl, char* lds, Issue&& issue, Read&& read,
                                          Mma&& mma) {
-  pipeline<G, RPM, false>(KT, nl, lds, issue, read, [](int, int, const char*) {}, mma);
+  pipeline<G, RPM, 0>(KT, nl, lds, issue, read, [](int, int, const char*) {}, mma);
 }
 
 }  // namespace ns

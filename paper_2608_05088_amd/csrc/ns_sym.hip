@@ -181,9 +181,9 @@ void ns_gemm_sym_kernel(NsArgs args) {
       }
     };
     bf16x8 fa[2][I], fb[2][J];
-    // Burst stages (off-diagonal tiles) issue their loads among the MFMAs
-    // after the barrier (the update is faster with them before).
-    pipeline<PG, 1, true>(
+    // Burst stages (off-diagonal tiles) issue all their loads among the MFMAs
+    // after the barrier.
+    pipeline<PG, 1, PG::LOADS>(
         K / PG::BK, NL, lds,
         [&](int kt, int i) {
           dma16(rsP, voff[i], (uint32_t)PL::soff(kt),

@@ -116,7 +116,9 @@ void ns_update_kernel(NsArgs args) {
       for (int e = 0; e < 4; ++e) acc[a][b][e] = 0.f;
   bf16x8 fx[2][NA], fb[2][NB];
 
-  pipeline<G, 1>(
+  // X stages (from further away) are issued right after each barrier, B'
+  // stages (L2-resident panels) from among the MFMAs that follow it.
+  pipeline<G, 1, LOADS / 2>(
       K / BK, LOADS, lds,
       [&](int kt, int q) {   // q < LOADS / 2: B' rows, else X k-rows
         const uint32_t la = lds_u32(lds + (kt % STAGES) * STAGE_BYTES + dst_off[q]);
@@ -135,6 +137,7 @@ void ns_update_kernel(NsArgs args) {
           fx[buf][a] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
         }
       },
+      [](int, int, const char*) {},
       [&](int buf, auto&& after) {
 #pragma unroll
         for (int a = 0; a < NA; ++a)
